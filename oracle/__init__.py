@@ -1,0 +1,212 @@
+"""CPU oracle for the FP8 linear layer with per-tensor power-of-two scaling biases.
+
+TEST INFRASTRUCTURE ONLY.  Plain, slow, obviously correct statement of what the
+GPU path computes (Perez et al., arXiv 2309.17224).  Only the tests, the smoke
+check and the benchmark's CPU-baseline leg may import this package; the library
+and its Python binding never do.  The arithmetic lives in ``fp8_oracle.c``
+(plain C, fp64); this module compiles it with gcc and wraps it with ctypes over
+numpy arrays (host memory, synchronous).
+
+Paper passages (section / equation / table):
+  * formats: App. A Eq. 4, Table 7, App. B special values
+  * ``amax`` and ``bias_from_amax``: Sec. 2.3 Eq. 3; margin Sec. 3.2
+  * ``cast``: Sec. 2.1 Eq. 1 (scale = x * 2^b), App. A (clip on overflow)
+  * ``gemm_nt``: Sec. 2 and 2.2 (FP8 x FP8, high-precision accumulate),
+    Sec. 2.1 Eq. 2 (unscale by -(b_a + b_b))
+  * ``ptq_quantise_weights``: Sec. 3.1
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "fp8_oracle.c")
+LIB = os.path.join(HERE, "liboracle.so")
+
+# format ids: E4M3 / E5M2 are the OCP formats, Table 7 rows "(b)";
+# E4_A / E5_A are the paper's default formats, Table 7 rows "(a)".
+E4M3, E5M2, E4_A, E5_A = 0, 1, 2, 3
+BF16, F32 = 0, 1
+FLAG_NONFINITE, FLAG_ZERO = 1, 2
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile fp8_oracle.c into liboracle.so with gcc (plain -O2, OpenMP)."""
+    if force or not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+        tmp = LIB + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-std=c11", "-O2", "-fopenmp", "-fPIC", "-shared", SRC, "-o", tmp, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, LIB)
+    return LIB
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+            build(force=True)
+        L = ctypes.CDLL(LIB)
+        vp, i32, i64, u32p = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.POINTER(ctypes.c_uint32)
+        L.oracle_fp8_decode.restype = ctypes.c_double
+        L.oracle_fp8_decode.argtypes = [ctypes.c_int, ctypes.c_int]
+        L.oracle_fp8_encode.restype = ctypes.c_int
+        L.oracle_fp8_encode.argtypes = [ctypes.c_int, ctypes.c_double]
+        L.oracle_fp8_max_num.restype = ctypes.c_double
+        L.oracle_fp8_max_num.argtypes = [ctypes.c_int]
+        L.oracle_amax.restype = None
+        L.oracle_amax.argtypes = [vp, ctypes.c_int, i64, u32p]
+        L.oracle_bias_from_amax.restype = i32
+        L.oracle_bias_from_amax.argtypes = [ctypes.c_uint32, ctypes.c_int, i32, u32p]
+        L.oracle_fp8_scale_bias.restype = i32
+        L.oracle_fp8_scale_bias.argtypes = [vp, ctypes.c_int, i64, ctypes.c_int, i32,
+                                            ctypes.POINTER(i32), u32p, u32p]
+        L.oracle_fp8_cast.restype = i32
+        L.oracle_fp8_cast.argtypes = [vp, ctypes.c_int, i64, i64, i64, ctypes.c_int, i32,
+                                      vp, i64, vp, i64]
+        L.oracle_gemm_nt.restype = i32
+        L.oracle_gemm_nt.argtypes = [vp, ctypes.c_int, i32, i64, vp, ctypes.c_int, i32, i64,
+                                     i64, i64, i64, vp, vp, ctypes.c_int, i64]
+        L.oracle_ptq_quantise_weights.restype = i32
+        L.oracle_ptq_quantise_weights.argtypes = [vp, ctypes.c_int, i64, i64, vp, vp,
+                                                  ctypes.POINTER(i32), u32p]
+        L.oracle_num_threads.restype = ctypes.c_int
+        L.oracle_set_num_threads.argtypes = [ctypes.c_int]
+        L.oracle_bf16_to_double.restype = ctypes.c_double
+        L.oracle_bf16_to_double.argtypes = [ctypes.c_uint16]
+        L.oracle_round_bf16.restype = ctypes.c_uint16
+        L.oracle_round_bf16.argtypes = [ctypes.c_double]
+        _lib = L
+    return _lib
+
+
+# ---------------------------------------------------------------- helpers
+def _hp(x: np.ndarray) -> tuple[np.ndarray, int]:
+    """Accept bf16 bit patterns (uint16) or float32; return (contiguous array, dtype id)."""
+    if x.dtype == np.uint16:
+        return np.ascontiguousarray(x), BF16
+    if x.dtype == np.float32:
+        return np.ascontiguousarray(x), F32
+    raise TypeError("oracle inputs are bf16 bit patterns (uint16) or float32, got %s" % x.dtype)
+
+
+def _ptr(a: np.ndarray | None):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def decode(fmt: int, code: int) -> float:
+    return lib().oracle_fp8_decode(fmt, int(code))
+
+
+def decode_table(fmt: int) -> np.ndarray:
+    return np.array([decode(fmt, c) for c in range(256)], dtype=np.float64)
+
+
+def encode(fmt: int, v: float) -> int:
+    return lib().oracle_fp8_encode(fmt, float(v))
+
+
+def max_num(fmt: int) -> float:
+    return lib().oracle_fp8_max_num(fmt)
+
+
+def amax_bits(x: np.ndarray) -> int:
+    x, dt = _hp(x)
+    out = ctypes.c_uint32(0)
+    lib().oracle_amax(_ptr(x), dt, x.size, ctypes.byref(out))
+    return out.value
+
+
+def bias_from_amax(amax_f32_bits: int, fmt: int, margin: int = 0) -> tuple[int, int]:
+    """Returns (bias, flags)."""
+    fl = ctypes.c_uint32(0)
+    b = lib().oracle_bias_from_amax(ctypes.c_uint32(amax_f32_bits), fmt, margin, ctypes.byref(fl))
+    return int(b), int(fl.value)
+
+
+def scale_bias(x: np.ndarray, fmt: int, margin: int = 0) -> tuple[int, int, int]:
+    """compute_bias of the paper: returns (bias, amax fp32 bits, flags)."""
+    x, dt = _hp(x)
+    b = ctypes.c_int32(0)
+    a = ctypes.c_uint32(0)
+    fl = ctypes.c_uint32(0)
+    st = lib().oracle_fp8_scale_bias(_ptr(x), dt, x.size, fmt, margin, ctypes.byref(b),
+                                     ctypes.byref(a), ctypes.byref(fl))
+    if st:
+        raise ValueError("oracle_fp8_scale_bias failed")
+    return int(b.value), int(a.value), int(fl.value)
+
+
+def cast(x: np.ndarray, fmt: int, bias: int, transpose: bool = False):
+    """Scale by 2^bias and cast to FP8 codes.  x is [rows, cols] (or 1-D).
+    Returns q (uint8, same shape) and, if transpose, qT ([cols, rows])."""
+    x, dt = _hp(x)
+    shp = x.shape if x.ndim == 2 else (1, x.size)
+    rows, cols = shp
+    q = np.empty(shp, dtype=np.uint8)
+    qT = np.empty((cols, rows), dtype=np.uint8) if transpose else None
+    st = lib().oracle_fp8_cast(_ptr(x), dt, rows, cols, cols, fmt, int(bias), _ptr(q), cols,
+                               _ptr(qT), rows)
+    if st:
+        raise ValueError("oracle_fp8_cast failed")
+    q = q.reshape(x.shape)
+    return (q, qT) if transpose else q
+
+
+def gemm_nt(a8: np.ndarray, fmt_a: int, ba: int, b8: np.ndarray, fmt_b: int, bb: int,
+            out_dt: int = F32, rows: np.ndarray | None = None) -> np.ndarray:
+    """out[r, j] = round(2^-(ba+bb) * sum_k dec(a8[i, k]) * dec(b8[j, k])), fp64 sum.
+    a8 is [M, K], b8 is [N, K] (uint8 codes).  If rows is given, only those rows
+    of a8 are used.  Returns float32, or bf16 bit patterns (uint16)."""
+    a8 = np.ascontiguousarray(a8, dtype=np.uint8)
+    b8 = np.ascontiguousarray(b8, dtype=np.uint8)
+    M, K = a8.shape
+    N, K2 = b8.shape
+    if K != K2:
+        raise ValueError("contraction sizes differ")
+    rr = None
+    if rows is not None:
+        rr = np.ascontiguousarray(rows, dtype=np.int64)
+        M = rr.size
+    out = np.empty((M, N), dtype=np.float32 if out_dt == F32 else np.uint16)
+    st = lib().oracle_gemm_nt(_ptr(a8), fmt_a, int(ba), K, _ptr(b8), fmt_b, int(bb), K,
+                              M, N, K, _ptr(rr), _ptr(out), out_dt, N)
+    if st:
+        raise ValueError("oracle_gemm_nt failed")
+    return out
+
+
+def ptq_quantise_weights(w: np.ndarray):
+    """Post-training quantisation of one [K, N] weight: returns (w8, w8t, bias, flags)."""
+    w, dt = _hp(w)
+    K, N = w.shape
+    w8 = np.empty((K, N), dtype=np.uint8)
+    w8t = np.empty((N, K), dtype=np.uint8)
+    b = ctypes.c_int32(0)
+    fl = ctypes.c_uint32(0)
+    st = lib().oracle_ptq_quantise_weights(_ptr(w), dt, K, N, _ptr(w8), _ptr(w8t),
+                                           ctypes.byref(b), ctypes.byref(fl))
+    if st:
+        raise ValueError("oracle_ptq_quantise_weights failed")
+    return w8, w8t, int(b.value), int(fl.value)
+
+
+def bf16_to_f64(h: int) -> float:
+    return lib().oracle_bf16_to_double(int(h))
+
+
+def round_bf16(y: float) -> int:
+    return int(lib().oracle_round_bf16(float(y)))
+
+
+def num_threads() -> int:
+    return int(lib().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    lib().oracle_set_num_threads(int(n))
