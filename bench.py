@@ -1,0 +1,240 @@
+#!/usr/bin/env python3
+"""Benchmark of the FP8 linear layer (amax + bias + cast + FP8 matmuls) on one GPU.
+
+A step is one pass of the whole path over one batch of a workload (see
+paper_2309_17224_amd.workloads): weight bias and cast, activation bias and
+cast, forward matmul with epilogue amax, gradient bias and cast (E5), grad-input
+matmul with epilogue amax, grad-weight matmul.  Inputs are synthetic, seeded,
+already resident in HBM when timing starts.
+
+Prints one JSON line:
+  value      = 6*M*N*K per linear (fwd + bwd matmul FLOPs) / step time, TFLOP/s
+  roofline   = the dominant kernel against its roofline, timed with HIP events
+  cpu_baseline = the CPU oracle on a bounded sample, extrapolated to one step
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+FP8_PEAK_TFLOPS = 5000.0     # MI355X dense FP8 MFMA, published
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, published
+METRIC = "FP8 linear fwd+bwd TFLOP/s incl. amax+cast, % of FP8 MFMA peak"
+DEFAULT_WORKLOAD = "llama2-7b-up"
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__)
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    p.add_argument("--margin", type=int, default=0)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-budget", type=float, default=12.0,
+                   help="seconds of oracle GEMM work in the CPU baseline sample")
+    p.add_argument("--flush-mb", type=int, default=0,
+                   help="write this many MB before every step (evicts the 256 MB MALL)")
+    return p.parse_args()
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def make_inputs(w):
+    from paper_2309_17224_amd import workloads as wl
+    t0 = time.time()
+    cpu = {t.name: wl.make_tensor(w, t.name) for t in w.tensors}
+    log(f"[bench] generated {len(cpu)} tensors in {time.time() - t0:.1f}s")
+    return cpu
+
+
+def time_steps(step, steps, warmup, flush=None):
+    import torch
+    for _ in range(warmup):
+        if flush is not None:
+            flush.add_(1)
+        step.run()
+    torch.cuda.synchronize()
+    ncalls = len(step.calls)
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(ncalls)] for _ in range(steps)]
+    fl_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+             for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(steps):
+        if flush is not None:
+            fl_ev[s][0].record()
+            flush.add_(1)
+            fl_ev[s][1].record()
+        for i, (_, _, _, fn) in enumerate(step.calls):
+            ev[s][i][0].record()
+            fn()
+            ev[s][i][1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_call = [[ev[s][i][0].elapsed_time(ev[s][i][1]) * 1e-3 for i in range(ncalls)]
+                for s in range(steps)]
+    flush_s = sum(a.elapsed_time(b) * 1e-3 for a, b in fl_ev) if flush is not None else 0.0
+    return wall, per_call, flush_s
+
+
+def roofline(step, per_call):
+    """Group per-call HIP-event durations by kernel kind; the dominant kind
+    (largest total time) is reported against its roofline."""
+    steps = len(per_call)
+    kinds = {}
+    for i, (label, kind, work, _) in enumerate(step.calls):
+        t = sum(per_call[s][i] for s in range(steps))
+        k = kinds.setdefault(kind, {"time": 0.0, "work": 0, "launches": 0})
+        k["time"] += t
+        k["work"] += work * steps
+        k["launches"] += steps
+    table = {}
+    for kind, k in kinds.items():
+        avg = k["time"] / k["launches"]
+        per_launch = k["work"] / k["launches"]
+        if kind.startswith("gemm"):
+            ach = per_launch / avg / 1e12 if avg > 0 else 0.0
+            table[kind] = dict(bound="mfma", achieved=ach, peak=FP8_PEAK_TFLOPS, unit="TFLOP/s",
+                               frac=ach / FP8_PEAK_TFLOPS, avg_us=avg * 1e6, per_launch=per_launch,
+                               total_ms=k["time"] / steps * 1e3)
+        elif kind in ("amax", "cast"):
+            ach = per_launch / avg / 1e9 if avg > 0 else 0.0
+            table[kind] = dict(bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s",
+                               frac=ach / HBM_PEAK_GBS, avg_us=avg * 1e6, per_launch=per_launch,
+                               total_ms=k["time"] / steps * 1e3)
+        else:
+            table[kind] = dict(avg_us=avg * 1e6, total_ms=k["time"] / steps * 1e3)
+    dom = max((k for k in table if "bound" in table[k]), key=lambda k: table[k]["total_ms"])
+    d = table[dom]
+    roof = {"bound": d["bound"], "achieved": round(d["achieved"], 2), "peak": d["peak"],
+            "unit": d["unit"], "frac": round(d["frac"], 4), "traffic": None,
+            "kernel": dom, "avg_launch_us": round(d["avg_us"], 2)}
+    return roof, table
+
+
+def cpu_baseline(w, cpu_tensors, budget_s):
+    """The oracle, as it is, on a bounded sample of one step: amax, bias and
+    cast on the full tensors, the matmuls on sampled rows, extrapolated
+    linearly in rows (every output row costs the same)."""
+    import numpy as np
+    import oracle as orc
+    from paper_2309_17224_amd import workloads as wl
+    bits = {k: wl.bf16_bits(v) for k, v in cpu_tensors.items()}
+    t_quant = 0.0
+    codes = {}
+    fmt_of = {}
+    for l in w.linears:
+        fmt_of.setdefault(l.w, orc.E4M3)
+        fmt_of.setdefault(l.x, orc.E4M3)
+        if w.train:
+            fmt_of.setdefault(l.dy, orc.E5M2)
+    for name, fmt in fmt_of.items():
+        t0 = time.perf_counter()
+        b, _, _ = orc.scale_bias(bits[name], fmt)
+        q, qT = orc.cast(bits[name], fmt, b, transpose=True)
+        t_quant += time.perf_counter() - t0
+        codes[name] = (q, qT, b, fmt)
+    gemms = []
+    for l in w.linears:
+        x, wq = codes[l.x], codes[l.w]
+        gemms.append(("fwd", x[0], x[3], x[2], wq[1], wq[3], wq[2], l.M))
+        if w.train:
+            g = codes[l.dy]
+            gemms.append(("dx", g[0], g[3], g[2], wq[0], wq[3], wq[2], l.M))
+            gemms.append(("dw", x[1], x[3], x[2], g[1], g[3], g[2], l.K))
+    # calibrate rows per matmul so that the sample costs about budget_s
+    per_row = []
+    for name, A, fa, ba, B, fb, bb, rows in gemms:
+        r = np.arange(min(4, rows))
+        t0 = time.perf_counter()
+        orc.gemm_nt(A, fa, ba, B, fb, bb, rows=r)
+        per_row.append((time.perf_counter() - t0) / len(r))
+    share = budget_s / max(1, len(gemms))
+    t_gemm = 0.0
+    sampled = []
+    for (name, A, fa, ba, B, fb, bb, rows), pr in zip(gemms, per_row):
+        nr = int(max(4, min(rows, share / max(pr, 1e-9))))
+        r = np.linspace(0, rows - 1, nr).astype(np.int64)
+        t0 = time.perf_counter()
+        orc.gemm_nt(A, fa, ba, B, fb, bb, rows=r)
+        dt = time.perf_counter() - t0
+        t_gemm += dt * rows / nr
+        sampled.append(f"{name}:{nr}/{rows} rows")
+    flops = sum(2 * l.M * l.N * l.K * (3 if w.train else 1) for l in w.linears)
+    total = t_quant + t_gemm
+    return {"value": round(flops / total / 1e12, 6), "unit": "TFLOP/s", "cores": orc.num_threads(),
+            "kind": "oracle",
+            "sample": "amax+bias+cast of every tensor in full (%.1fs); matmuls on %s, fp64 "
+                      "accumulation, extrapolated by rows to %.1fs" % (t_quant, ", ".join(sampled),
+                                                                     t_gemm)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus %d is not supported"
+                          % args.gpus}))
+        sys.exit(2)
+    import torch
+    from paper_2309_17224_amd import fp8lin
+    from paper_2309_17224_amd import linear as L
+    from paper_2309_17224_amd import workloads as wl
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    fp8lin.lib()  # fails loudly when the HIP library is missing
+    w = wl.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    cpu = make_inputs(w)
+    tens = {k: v.to(dev) for k, v in cpu.items()}
+    torch.cuda.synchronize()
+    step = L.WorkloadStep(w, tens, dev, margin=args.margin)
+    if not w.train:
+        step.prepare_inference()
+    flush = None
+    if args.flush_mb:
+        flush = torch.zeros(args.flush_mb * (1 << 20) // 4, dtype=torch.float32, device=dev)
+    log(f"[bench] {w.name}: {len(step.calls)} calls per step; warmup {args.warmup}, steps {args.steps}")
+    wall, per_call, flush_s = time_steps(step, args.steps, args.warmup, flush)
+    step_s = (wall - flush_s) / args.steps
+    flops = step.gemm_flops()
+    value = flops / step_s / 1e12
+    roof, table = roofline(step, per_call)
+    for kind, d in sorted(table.items()):
+        log(f"[bench] {kind:9s} " + " ".join(f"{k}={v:.4g}" if isinstance(v, float) else f"{k}={v}"
+                                             for k, v in d.items()))
+    out = {
+        "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_s * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "fp8",
+        "data": "synthetic",
+        "config": {"workload": w.name, "description": w.description,
+                   "linears": [dict(name=l.name, M=l.M, K=l.K, N=l.N) for l in w.linears],
+                   "mode": "train fwd+bwd" if w.train else "PTQ inference fwd",
+                   "accumulate": "fp32", "outputs": "Y,dX bf16; dW fp32",
+                   "margin": args.margin, "mall_flush_mb": args.flush_mb},
+        "frac_of_fp8_peak": round(value / FP8_PEAK_TFLOPS, 4),
+        "roofline": roof,
+        "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv) for kk, vv in d.items()}
+                    for k, d in table.items()},
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline(w, cpu, args.cpu_budget)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

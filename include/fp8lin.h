@@ -1,0 +1,198 @@
+/*
+ * fp8lin.h -- C ABI of libfp8lin.so: the FP8 linear layer with dynamically
+ * computed per-tensor power-of-two scaling biases, for AMD MI355X (gfx950).
+ *
+ * Method: Perez et al., "Training and inference of large language models
+ * using 8-bit floating point" (arXiv 2309.17224).
+ *   Sec. 2.3 Eq. 3   amax = max|T|, scaling bias b = floor(log2(max_num / amax))
+ *   Sec. 2.1 Eq. 1   scaling = adding b to the exponent = multiplying by 2^b
+ *                    before the cast to FP8
+ *   Sec. 2.1 Eq. 2   after the FP8 matmul the output is unscaled by
+ *                    -(b_w + b_x)
+ *   Sec. 2.2         gradients use FP8 E5, weights and activations FP8 E4;
+ *                    the backward pass has two FP8 matmuls (grad-input and
+ *                    grad-weight), each unscaled by its inputs' biases
+ *   Sec. 3           FP8-AMAX: one bias per tensor per call; Sec. 3.2 margin
+ *   Sec. 3.1         post-training quantisation: weight bias computed once
+ *
+ * FP8 formats.  The matrix cores of gfx950 consume the OCP formats E4M3 and
+ * E5M2, which are the "(b)" rows of Table 7 (App. A): E4M3 bias 7, max 448,
+ * NaN = S.1111.111, no infinity; E5M2 bias 15, max 57344, IEEE infinities
+ * and NaNs.  The paper's default "(a)" formats (bias 8 / 16, NaN = 0x80) are
+ * not produced by this library.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Every data pointer is a DEVICE pointer owned by the caller.  The library
+ *    never allocates, frees or keeps memory, and never synchronises.
+ *  - Every call is asynchronous on `stream` (a hipStream_t passed as void*;
+ *    NULL is the null stream).
+ *  - Arguments are checked on the host before anything is launched.  A call
+ *    that returns an error has launched nothing.
+ *  - Scaling biases are int32 in device memory, so amax -> bias -> cast ->
+ *    matmul needs no copy to the host.
+ *  - Numerical conditions are never errors.  *flags (optional, uint32 in
+ *    device memory) is overwritten by fp8_scale_bias / ptq_quantise_weights
+ *    with FP8_FLAG_NONFINITE when the amax is NaN or infinite and with
+ *    FP8_FLAG_ZERO when it is zero; the bias is then 0.
+ *  - Layouts are dense row-major unless a leading dimension (ld*, in
+ *    elements) is given.
+ *  - Rounding of the cast is to nearest, ties to even; values beyond the
+ *    largest finite FP8 value, infinities included, clip to it with their
+ *    sign (App. A); NaN becomes 0x7F with the input's sign bit.
+ *  - Matmul accumulation is fp32 (MFMA); the unscale 2^-(b_a + b_b) is applied
+ *    to the fp32 sum, which is then rounded once to the output type.
+ *  - Thread safety: calls hold no state and may be issued from any thread.
+ */
+#ifndef FP8LIN_H
+#define FP8LIN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define FP8_OK 0       /* launched (or nothing to do) */
+#define FP8_EINVAL 1   /* bad argument: null pointer, negative or too large size,
+                          leading dimension below the row length, misaligned
+                          pointer, unknown format or dtype, workspace too small */
+#define FP8_ENOTSUP 2  /* valid but unsupported combination */
+#define FP8_EHIP 3     /* the HIP runtime reported a launch error */
+
+/* FP8 formats (OCP; Table 7 rows "(b)"). */
+#define FP8_E4M3 0
+#define FP8_E5M2 1
+
+/* Higher-precision element types of inputs and outputs. */
+#define FP8_DT_BF16 0
+#define FP8_DT_F32 1
+
+/* Bits of *flags. */
+#define FP8_FLAG_NONFINITE 1u
+#define FP8_FLAG_ZERO 2u
+
+/* Largest accepted |margin|. */
+#define FP8_MAX_MARGIN 65536
+
+/* Text for a status code (static storage, never NULL). */
+const char *fp8_status_string(int32_t status);
+
+/* Version of this ABI (incremented on any incompatible change). */
+int32_t fp8_abi_version(void);
+
+/* Workspace bytes fp8_scale_bias needs for n elements (0 when n == 0). */
+size_t fp8_scale_bias_ws_bytes(int64_t n);
+
+/*
+ * fp8_scale_bias -- the compute_bias step of FP8-AMAX (Sec. 2.3 Eq. 3, Sec. 3).
+ *   amax = max_i |x_i| over all n elements (one tensor, one call), then
+ *   *bias = floor(log2(max_num(fmt) / amax)) - margin,
+ *   evaluated exactly: *bias is the largest integer b with amax * 2^b <= max_num,
+ *   minus the margin.  max_num is 448 (E4M3) or 57344 (E5M2).
+ * x:         n elements of type dt (FP8_DT_BF16 or FP8_DT_F32), aligned to the
+ *            element size.  -0 counts as 0; a NaN makes the amax NaN.
+ * margin:    subtracted from the bias (Sec. 3.2: 3 was used with FP16
+ *            accumulation; 0 with fp32 accumulation).  |margin| <= FP8_MAX_MARGIN.
+ * bias:      out, one int32 (device).
+ * amax_bits: out, optional: the fp32 bit pattern of the amax (device).
+ * flags:     out, optional: see the conventions above (device).
+ * ws:        device workspace of at least fp8_scale_bias_ws_bytes(n) bytes,
+ *            4-byte aligned; its contents are scratch.  Concurrent calls need
+ *            distinct workspaces.
+ * n == 0 gives amax 0, bias 0 and FP8_FLAG_ZERO.
+ */
+int32_t fp8_scale_bias(const void *x, int32_t dt, int64_t n, int32_t fmt, int32_t margin,
+                       int32_t *bias, uint32_t *amax_bits, uint32_t *flags,
+                       void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * fp8_bias_from_amax -- Eq. 3 from an amax already in device memory (for
+ * example one produced by a matmul epilogue, see fp8_linear_fwd).
+ * amax_bits: in, fp32 bit pattern (sign ignored).  Outputs as fp8_scale_bias.
+ */
+int32_t fp8_bias_from_amax(const uint32_t *amax_bits, int32_t fmt, int32_t margin,
+                           int32_t *bias, uint32_t *flags, void *stream);
+
+/*
+ * fp8_cast_e4 / fp8_cast_e5 -- scale and cast (Sec. 2.1 Eq. 1; E4 for weights
+ * and activations, E5 for gradients, Sec. 2.2):
+ *   q[r, c] = RNE_saturate_fmt(x[r, c] * 2^(*bias))
+ * The product is exact (a power-of-two scale of a bf16/fp32 value), so the
+ * cast is the only rounding.
+ * x:    [rows, cols] of type dt, row stride ldx >= cols elements.
+ * bias: in, one int32 (device), e.g. written by fp8_scale_bias.
+ * q:    out, [rows, cols] uint8 codes, row stride ldq >= cols; may be NULL
+ *       if qT is given.
+ * qT:   out, optional, the same codes transposed: [cols, rows], row stride
+ *       ldqT >= rows.  The matmuls below take this copy where they contract
+ *       over the rows of a tensor.
+ * rows == 0 or cols == 0 is a no-op.
+ */
+int32_t fp8_cast_e4(const void *x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx,
+                    const int32_t *bias, uint8_t *q, int64_t ldq, uint8_t *qT, int64_t ldqT,
+                    void *stream);
+int32_t fp8_cast_e5(const void *x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx,
+                    const int32_t *bias, uint8_t *q, int64_t ldq, uint8_t *qT, int64_t ldqT,
+                    void *stream);
+
+/*
+ * fp8_linear_fwd -- forward FP8 matmul with unscale (Sec. 2, Eq. 2):
+ *   Y[m, n] = 2^-(bx + bw) * sum_k X8[m, k] * W8[k, n]
+ * x8:  [M, K] E4M3 codes (dense), bias *bx.
+ * w8t: [N, K] E4M3 codes: the weight [K, N] stored transposed (qT of its cast),
+ *      bias *bw.
+ * y:   out, [M, N] dense, y_dt = FP8_DT_BF16 or FP8_DT_F32.
+ * y_amax_bits: optional out: if given, the fp32 bit pattern of max|Y| (of
+ *      the rounded outputs) is written there, so that the next layer can take
+ *      its bias with fp8_bias_from_amax instead of reading Y again.
+ * M == 0 or N == 0 is a no-op; K == 0 writes zeros.
+ * Pointers must be 16-byte aligned.
+ */
+int32_t fp8_linear_fwd(const uint8_t *x8, const int32_t *bx, const uint8_t *w8t, const int32_t *bw,
+                       void *y, int32_t y_dt, int64_t M, int64_t N, int64_t K,
+                       uint32_t *y_amax_bits, void *stream);
+
+/*
+ * fp8_linear_bwd_dx -- grad-input FP8 matmul (Sec. 2.2):
+ *   dX[m, k] = 2^-(bg + bw) * sum_n dY8[m, n] * W8[k, n]
+ * dy8: [M, N] E5M2 codes, bias *bg.   w8: [K, N] E4M3 codes, bias *bw.
+ * dx:  out, [M, K], dx_dt.   dx_amax_bits: optional, as in fp8_linear_fwd.
+ */
+int32_t fp8_linear_bwd_dx(const uint8_t *dy8, const int32_t *bg, const uint8_t *w8,
+                          const int32_t *bw, void *dx, int32_t dx_dt, int64_t M, int64_t N,
+                          int64_t K, uint32_t *dx_amax_bits, void *stream);
+
+/*
+ * fp8_linear_bwd_dw -- grad-weight FP8 matmul (Sec. 2.2):
+ *   dW[k, n] = 2^-(bx + bg) * sum_m X8[m, k] * dY8[m, n]
+ * x8t:  [K, M] E4M3 codes: X8 transposed (qT of the activation cast), bias *bx.
+ * dy8t: [N, M] E5M2 codes: dY8 transposed (qT of the gradient cast), bias *bg.
+ * dw:   out, [K, N], dw_dt (fp32 recommended: it feeds the weight update).
+ */
+int32_t fp8_linear_bwd_dw(const uint8_t *x8t, const int32_t *bx, const uint8_t *dy8t,
+                          const int32_t *bg, void *dw, int32_t dw_dt, int64_t M, int64_t N,
+                          int64_t K, void *stream);
+
+/*
+ * ptq_quantise_weights -- post-training quantisation of one weight tensor
+ * (Sec. 3.1): the bias is computed once from the whole tensor, then the
+ * weight is scaled and cast to E4M3.
+ * w:   [K, N] of type dt (dense).
+ * w8:  out, optional, [K, N] E4M3 codes (operand of fp8_linear_bwd_dx).
+ * w8t: out, optional, [N, K] E4M3 codes (operand of fp8_linear_fwd).
+ *      At least one of w8 / w8t must be given.
+ * bw:  out, the weight's bias (device).  flags: optional, as fp8_scale_bias.
+ * ws:  workspace of fp8_scale_bias_ws_bytes(K * N) bytes.
+ */
+int32_t ptq_quantise_weights(const void *w, int32_t dt, int64_t K, int64_t N, uint8_t *w8,
+                             uint8_t *w8t, int32_t *bw, uint32_t *flags, void *ws,
+                             size_t ws_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FP8LIN_H */

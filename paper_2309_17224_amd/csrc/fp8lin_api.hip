@@ -1,0 +1,128 @@
+// C entry points of libfp8lin.so (declared and documented in fp8lin.h).
+// Each call checks its arguments on the host, then enqueues kernels on the
+// caller's stream; nothing is allocated, kept or synchronised.
+#include "fp8lin_internal.h"
+
+using namespace fp8lin;
+
+namespace {
+
+constexpr int64_t kMaxDim = (int64_t)1 << 40;
+
+bool fmt_ok(int32_t f) { return f == FP8_E4M3 || f == FP8_E5M2; }
+bool dt_ok(int32_t d) { return d == FP8_DT_BF16 || d == FP8_DT_F32; }
+int esize(int32_t d) { return d == FP8_DT_BF16 ? 2 : 4; }
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+hipStream_t as_stream(void* s) { return (hipStream_t)s; }
+
+int32_t cast_common(const void* x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx,
+                    const int32_t* bias, uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT,
+                    int fmt, void* stream) {
+    if (!dt_ok(dt) || rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return FP8_EINVAL;
+    if (rows == 0 || cols == 0) return FP8_OK;
+    if (!x || !bias || (!q && !qT)) return FP8_EINVAL;
+    if (!aligned(x, esize(dt)) || !aligned(bias, 4)) return FP8_EINVAL;
+    if (ldx < cols || (q && ldq < cols) || (qT && ldqT < rows)) return FP8_EINVAL;
+    return launch_cast(x, dt, rows, cols, ldx, fmt, bias, q, ldq, qT, ldqT, as_stream(stream));
+}
+
+int32_t gemm_common(const uint8_t* a, int fa, const int32_t* ba, const uint8_t* b, int fb,
+                    const int32_t* bb, void* c, int32_t c_dt, int64_t M, int64_t N, int64_t K,
+                    uint32_t* amax, void* stream) {
+    if (!dt_ok(c_dt) || M < 0 || N < 0 || K < 0 || M > kMaxDim || N > kMaxDim || K > kMaxDim)
+        return FP8_EINVAL;
+    if (M == 0 || N == 0) return FP8_OK;
+    if (!c || !ba || !bb || (K > 0 && (!a || !b))) return FP8_EINVAL;
+    if (!aligned(c, esize(c_dt)) || !aligned(ba, 4) || !aligned(bb, 4)) return FP8_EINVAL;
+    if (amax && !aligned(amax, 4)) return FP8_EINVAL;
+    if (M > INT32_MAX || N > INT32_MAX) return FP8_ENOTSUP;
+    return launch_gemm_nt(a, fa, ba, b, fb, bb, c, c_dt, M, N, K, amax, as_stream(stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* fp8_status_string(int32_t status) {
+    switch (status) {
+        case FP8_OK: return "ok";
+        case FP8_EINVAL: return "invalid argument";
+        case FP8_ENOTSUP: return "unsupported argument combination";
+        case FP8_EHIP: return "HIP launch error";
+        default: return "unknown status";
+    }
+}
+
+int32_t fp8_abi_version(void) { return 1; }
+
+size_t fp8_scale_bias_ws_bytes(int64_t n) {
+    if (n <= 0) return 0;
+    return (size_t)amax_blocks(n) * sizeof(uint32_t);
+}
+
+int32_t fp8_scale_bias(const void* x, int32_t dt, int64_t n, int32_t fmt, int32_t margin,
+                       int32_t* bias, uint32_t* amax_bits, uint32_t* flags, void* ws,
+                       size_t ws_bytes, void* stream) {
+    if (!dt_ok(dt) || !fmt_ok(fmt) || n < 0 || n > kMaxDim * 64) return FP8_EINVAL;
+    if (margin < -FP8_MAX_MARGIN || margin > FP8_MAX_MARGIN) return FP8_EINVAL;
+    if (!bias || !aligned(bias, 4)) return FP8_EINVAL;
+    if ((amax_bits && !aligned(amax_bits, 4)) || (flags && !aligned(flags, 4))) return FP8_EINVAL;
+    if (n > 0) {  // an empty tensor has amax 0: no input or workspace is read
+        if (!x || !aligned(x, esize(dt))) return FP8_EINVAL;
+        if (!ws || !aligned(ws, 4) || ws_bytes < fp8_scale_bias_ws_bytes(n)) return FP8_EINVAL;
+    }
+    return launch_scale_bias(x, dt, n, fmt, margin, bias, amax_bits, flags, (uint32_t*)ws,
+                             as_stream(stream));
+}
+
+int32_t fp8_bias_from_amax(const uint32_t* amax_bits, int32_t fmt, int32_t margin, int32_t* bias,
+                           uint32_t* flags, void* stream) {
+    if (!fmt_ok(fmt) || margin < -FP8_MAX_MARGIN || margin > FP8_MAX_MARGIN) return FP8_EINVAL;
+    if (!amax_bits || !bias || !aligned(amax_bits, 4) || !aligned(bias, 4)) return FP8_EINVAL;
+    if (flags && !aligned(flags, 4)) return FP8_EINVAL;
+    return launch_bias_from_amax(amax_bits, fmt, margin, bias, flags, as_stream(stream));
+}
+
+int32_t fp8_cast_e4(const void* x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx,
+                    const int32_t* bias, uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT,
+                    void* stream) {
+    return cast_common(x, dt, rows, cols, ldx, bias, q, ldq, qT, ldqT, FP8_E4M3, stream);
+}
+
+int32_t fp8_cast_e5(const void* x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx,
+                    const int32_t* bias, uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT,
+                    void* stream) {
+    return cast_common(x, dt, rows, cols, ldx, bias, q, ldq, qT, ldqT, FP8_E5M2, stream);
+}
+
+int32_t fp8_linear_fwd(const uint8_t* x8, const int32_t* bx, const uint8_t* w8t, const int32_t* bw,
+                       void* y, int32_t y_dt, int64_t M, int64_t N, int64_t K,
+                       uint32_t* y_amax_bits, void* stream) {
+    return gemm_common(x8, FP8_E4M3, bx, w8t, FP8_E4M3, bw, y, y_dt, M, N, K, y_amax_bits, stream);
+}
+
+int32_t fp8_linear_bwd_dx(const uint8_t* dy8, const int32_t* bg, const uint8_t* w8,
+                          const int32_t* bw, void* dx, int32_t dx_dt, int64_t M, int64_t N,
+                          int64_t K, uint32_t* dx_amax_bits, void* stream) {
+    // dX [M, K] = dY8 [M, N] . W8 [K, N]^T: contraction over N.
+    return gemm_common(dy8, FP8_E5M2, bg, w8, FP8_E4M3, bw, dx, dx_dt, M, K, N, dx_amax_bits, stream);
+}
+
+int32_t fp8_linear_bwd_dw(const uint8_t* x8t, const int32_t* bx, const uint8_t* dy8t,
+                          const int32_t* bg, void* dw, int32_t dw_dt, int64_t M, int64_t N,
+                          int64_t K, void* stream) {
+    // dW [K, N] = X8T [K, M] . dY8T [N, M]^T: contraction over M.
+    return gemm_common(x8t, FP8_E4M3, bx, dy8t, FP8_E5M2, bg, dw, dw_dt, K, N, M, nullptr, stream);
+}
+
+int32_t ptq_quantise_weights(const void* w, int32_t dt, int64_t K, int64_t N, uint8_t* w8,
+                             uint8_t* w8t, int32_t* bw, uint32_t* flags, void* ws, size_t ws_bytes,
+                             void* stream) {
+    if (!dt_ok(dt) || K < 0 || N < 0 || K > kMaxDim || N > kMaxDim) return FP8_EINVAL;
+    if (!bw || (!w8 && !w8t)) return FP8_EINVAL;
+    int32_t st = fp8_scale_bias(w, dt, K * N, FP8_E4M3, 0, bw, nullptr, flags, ws, ws_bytes, stream);
+    if (st != FP8_OK || K == 0 || N == 0) return st;
+    return cast_common(w, dt, K, N, N, bw, w8, N, w8t, K, FP8_E4M3, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,372 @@
+// FP8 x FP8 -> fp32 matmul with the unscale 2^-(b_a + b_b) fused into the
+// epilogue (Sec. 2 and 2.2; Eq. 2), for gfx950 matrix cores.
+//
+// C[m, n] = 2^-(ba + bb) * sum_k A[m, k] * B[n, k]   ("NT": both operands
+// are contiguous along the contraction index).  The forward pass, the
+// grad-input and the grad-weight products of the linear layer are all of
+// this form once the casts have written the transposed copies they need.
+//
+// Main kernel (K a multiple of 128, 16-byte aligned operands):
+//  * 256 x 256 output tile per workgroup of 4 waves; each wave owns a
+//    128 x 128 sub-tile = 8 x 8 blocks of v_mfma_f32_16x16x128_f8f6f4.
+//  * K advances 128 bytes at a time; both operand tiles (256 rows x 128 B)
+//    go HBM/L2 -> LDS with global_load_lds_dwordx4 (no VGPR staging) into a
+//    double buffer (2 x 64 KiB), so loads of step k+1 overlap the MFMAs of
+//    step k.
+//  * LDS rows are 128 B; the 16-byte chunk index is XOR-swizzled with the row
+//    (chunk ^ (row & 7)) by choosing which global chunk each lane fetches, so
+//    the fragment reads (ds_read_b128) are free of bank conflicts.
+//  * A fragment of the 16x16x128 MFMA is 32 bytes per lane: row (lane % 16),
+//    32 consecutive k of group (lane / 16).  The matrix core pairs the same
+//    register bytes of both operands, so any k order that is the same for
+//    both operands gives the same dot products.
+//  * The MFMA gets the B fragment as its first operand, so each lane's four
+//    accumulators are four consecutive n of one m: the epilogue writes 8 B
+//    (bf16) or 16 B (fp32) per lane.
+//  * Workgroup -> tile mapping: workgroups are dealt round-robin to the 8
+//    XCDs; the remap gives each XCD a contiguous range of tiles, walked in
+//    groups of 8 tile-rows, so tiles sharing operand panels meet in the same
+//    L2.
+// Fallback kernel (any K or alignment): 64 x 64 tiles, byte loads with
+// bounds checks and zero fill, same MFMA and epilogue.
+#include "fp8lin_internal.h"
+
+namespace fp8lin {
+namespace {
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// MFMA operand format selectors: 0 = fp8 (E4M3), 1 = bf8 (E5M2).
+template <int F0, int F1>
+__device__ __forceinline__ v4f mfma16(v8i a, v8i b, v4f c) {
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, F0, F1, 0, 0, 0, 0);
+}
+
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return 0x7FC0u;
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, off, 64));
+    return v;
+}
+
+// Direct HBM/L2 -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4):
+// lane i's 16 bytes land at lds_row + 16 i.  lds_row must be the same for the
+// whole wave.  The instruction is issued from inline assembly so that the
+// compiler does not treat every later LDS read as dependent on it (it cannot
+// tell the two halves of the double buffer apart and would wait for the
+// prefetch before each read); completion is tracked with wait_vmcnt below.
+__device__ __forceinline__ void lds_dma16(const uint8_t* g, uint32_t lds_row) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :
+                 : "s"(lds_row), "v"(g)
+                 : "memory");
+}
+
+// 32-bit LDS address of a pointer into a __shared__ array.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
+}
+
+// Wait until at most N vector-memory operations of this wave are in flight.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
+// Contiguous tile ranges per XCD, then grouped row-major order inside.
+__device__ __forceinline__ void tile_of(int b, int nb, int tiles_m, int tiles_n, int& tm, int& tn) {
+    const int x = b & 7, l = b >> 3;
+    const int per = nb >> 3, rem = nb & 7;
+    const int t = x * per + min(x, rem) + l;
+    constexpr int G = 8;
+    const int group = G * tiles_n;
+    const int gid = t / group;
+    const int first = gid * G;
+    const int gm = min(tiles_m - first, G);
+    const int r = t - gid * group;
+    tm = first + r % gm;
+    tn = r / gm;
+}
+
+// Store 4 consecutive outputs of row m starting at column n (unscaled by
+// 2^-sh); returns the largest output magnitude pattern (as fp32 bits).
+template <int OUT_DT>
+__device__ __forceinline__ uint32_t store4(void* C, int64_t ldc, int64_t m, int64_t n, int64_t M,
+                                           int64_t N, v4f acc, int sh, bool vec) {
+    float y[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) y[v] = ldexpf(acc[v], sh);
+    uint32_t mx = 0;
+    if (OUT_DT == FP8_DT_BF16) {
+        uint32_t h[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            h[v] = f32_to_bf16_rne(y[v]);
+            mx = max(mx, (h[v] & 0x7FFFu) << 16);
+        }
+        if (m < M) {
+            uint16_t* p = (uint16_t*)C + m * ldc + n;
+            if (vec && n + 3 < N) {
+                *(uint2*)p = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+            } else {
+                for (int v = 0; v < 4; ++v)
+                    if (n + v < N) p[v] = (uint16_t)h[v];
+            }
+        }
+    } else {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) mx = max(mx, __float_as_uint(y[v]) & 0x7FFFFFFFu);
+        if (m < M) {
+            float* p = (float*)C + m * ldc + n;
+            if (vec && n + 3 < N) {
+                *(float4*)p = make_float4(y[0], y[1], y[2], y[3]);
+            } else {
+                for (int v = 0; v < 4; ++v)
+                    if (n + v < N) p[v] = y[v];
+            }
+        }
+    }
+    return m < M ? mx : 0u;
+}
+
+// ------------------------------------------------------------ main kernel
+constexpr int kBM = 256, kBN = 256, kBK = 128, kThreads = 256;
+constexpr int kTileBytes = kBM * kBK;  // one operand tile, 32 KiB
+
+template <int FA, int FB, int OUT_DT, bool AMAX>
+__global__ __launch_bounds__(kThreads) void gemm_nt_256(
+    const uint8_t* __restrict__ A, const uint8_t* __restrict__ B, const int32_t* __restrict__ ba_p,
+    const int32_t* __restrict__ bb_p, void* __restrict__ C, int M, int N, int K, int tiles_m,
+    int tiles_n, int vec_out, uint32_t* __restrict__ amax_out) {
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * 2 * kTileBytes];
+
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    int tm, tn;
+    tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
+    const int m0 = tm * kBM, n0 = tn * kBN;
+
+    // Loader: wave w fills rows [64 w, 64 w + 64) of both tiles, 8 rows per
+    // instruction; lane -> row (lane / 8), physical chunk (lane % 8), which
+    // holds logical chunk (lane % 8) ^ (row % 8).
+    const int lrow = lane >> 3;
+    const int lchunk = (lane & 7) ^ lrow;
+    const uint8_t* a_src[8];
+    const uint8_t* b_src[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int ra = min(m0 + w * 64 + i * 8 + lrow, M - 1);
+        const int rb = min(n0 + w * 64 + i * 8 + lrow, N - 1);
+        a_src[i] = A + (int64_t)ra * K + lchunk * 16;
+        b_src[i] = B + (int64_t)rb * K + lchunk * 16;
+    }
+
+    // LDS row address of this wave's first loader row (wave-uniform).
+    const uint32_t lds_w = __builtin_amdgcn_readfirstlane(lds_addr(smem) + w * 64 * kBK);
+    auto issue = [&](int stage, int k0) {
+        const uint32_t la = lds_w + stage * 2 * kTileBytes;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            lds_dma16(a_src[i] + k0, la + i * 8 * kBK);
+            lds_dma16(b_src[i] + k0, la + kTileBytes + i * 8 * kBK);
+        }
+    };
+
+    const int wm = w >> 1, wn = w & 1;
+    const int frow = lane & 15, fg = lane >> 4;
+    // byte offsets (within a tile) of this lane's two 16-byte fragment pieces
+    const int fo0 = frow * kBK + (((2 * fg) ^ (frow & 7)) << 4);
+    const int fo1 = frow * kBK + (((2 * fg + 1) ^ (frow & 7)) << 4);
+
+    v4f acc[8][8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+
+    const int nk = K / kBK;
+    if (nk > 0) issue(0, 0);
+    for (int kt = 0; kt < nk; ++kt) {
+        const int st = kt & 1;
+        if (kt + 1 < nk) {
+            issue(st ^ 1, (kt + 1) * kBK);
+            wait_vmcnt<16>();
+        } else {
+            wait_vmcnt<0>();
+        }
+        __syncthreads();
+        const uint8_t* sa = smem + st * 2 * kTileBytes + wm * 128 * kBK;
+        const uint8_t* sb = smem + st * 2 * kTileBytes + kTileBytes + wn * 128 * kBK;
+        v8i bf[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const uint4 p0 = *(const uint4*)(sb + j * 16 * kBK + fo0);
+            const uint4 p1 = *(const uint4*)(sb + j * 16 * kBK + fo1);
+            bf[j] = v8i{(int)p0.x, (int)p0.y, (int)p0.z, (int)p0.w, (int)p1.x, (int)p1.y, (int)p1.z, (int)p1.w};
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const uint4 p0 = *(const uint4*)(sa + i * 16 * kBK + fo0);
+            const uint4 p1 = *(const uint4*)(sa + i * 16 * kBK + fo1);
+            const v8i af = v8i{(int)p0.x, (int)p0.y, (int)p0.z, (int)p0.w, (int)p1.x, (int)p1.y, (int)p1.z, (int)p1.w};
+#pragma unroll
+            for (int j = 0; j < 8; ++j) acc[i][j] = mfma16<FB, FA>(bf[j], af, acc[i][j]);
+        }
+        __syncthreads();
+    }
+
+    const int sh = -(*ba_p + *bb_p);
+    uint32_t mx = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int64_t m = m0 + wm * 128 + i * 16 + frow;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int64_t n = n0 + wn * 128 + j * 16 + fg * 4;
+            mx = max(mx, store4<OUT_DT>(C, N, m, n, M, N, acc[i][j], sh, vec_out != 0));
+        }
+    }
+    if (AMAX) {
+        mx = wave_max_u32(mx);
+        if (lane == 0) atomicMax(amax_out, mx);
+    }
+}
+
+// ------------------------------------------------------------ fallback kernel
+constexpr int kSBM = 64, kSBN = 64;
+
+template <int FA, int FB, int OUT_DT, bool AMAX>
+__global__ __launch_bounds__(kThreads) void gemm_nt_small(
+    const uint8_t* __restrict__ A, const uint8_t* __restrict__ B, const int32_t* __restrict__ ba_p,
+    const int32_t* __restrict__ bb_p, void* __restrict__ C, int64_t M, int64_t N, int64_t K,
+    int64_t tiles_n, int vec_out, uint32_t* __restrict__ amax_out) {
+    __shared__ __attribute__((aligned(16))) uint8_t sa[kSBM * kBK];
+    __shared__ __attribute__((aligned(16))) uint8_t sb[kSBN * kBK];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int64_t m0 = (blockIdx.x / tiles_n) * kSBM, n0 = (blockIdx.x % tiles_n) * kSBN;
+    // loader: thread -> row (tid / 4), logical chunks 2 (tid % 4), +1
+    const int lr = threadIdx.x >> 2, lq = threadIdx.x & 3;
+    const int wm = w >> 1, wn = w & 1;
+    const int frow = lane & 15, fg = lane >> 4;
+    const int fo0 = frow * kBK + (((2 * fg) ^ (frow & 7)) << 4);
+    const int fo1 = frow * kBK + (((2 * fg + 1) ^ (frow & 7)) << 4);
+
+    v4f acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+
+    for (int64_t k0 = 0; k0 < K; k0 += kBK) {
+#pragma unroll
+        for (int op = 0; op < 2; ++op) {
+            const uint8_t* src = op == 0 ? A : B;
+            const int64_t r = (op == 0 ? m0 : n0) + lr;
+            const int64_t rmax = op == 0 ? M : N;
+            uint8_t* dst = op == 0 ? sa : sb;
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int c = 2 * lq + h;  // logical 16-byte chunk
+                uint32_t wv[4] = {0, 0, 0, 0};
+                for (int t = 0; t < 16; ++t) {
+                    const int64_t k = k0 + c * 16 + t;
+                    uint32_t byte = 0;
+                    if (r < rmax && k < K) byte = src[r * K + k];
+                    wv[t >> 2] |= byte << (8 * (t & 3));
+                }
+                *(uint4*)(dst + lr * kBK + ((c ^ (lr & 7)) << 4)) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+            }
+        }
+        __syncthreads();
+        v8i bf[2], af[2];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const uint8_t* p = sb + (wn * 32 + j * 16) * kBK;
+            const uint4 p0 = *(const uint4*)(p + fo0), p1 = *(const uint4*)(p + fo1);
+            bf[j] = v8i{(int)p0.x, (int)p0.y, (int)p0.z, (int)p0.w, (int)p1.x, (int)p1.y, (int)p1.z, (int)p1.w};
+            const uint8_t* q = sa + (wm * 32 + j * 16) * kBK;
+            const uint4 q0 = *(const uint4*)(q + fo0), q1 = *(const uint4*)(q + fo1);
+            af[j] = v8i{(int)q0.x, (int)q0.y, (int)q0.z, (int)q0.w, (int)q1.x, (int)q1.y, (int)q1.z, (int)q1.w};
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) acc[i][j] = mfma16<FB, FA>(bf[j], af[i], acc[i][j]);
+        __syncthreads();
+    }
+
+    const int sh = -(*ba_p + *bb_p);
+    uint32_t mx = 0;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int64_t m = m0 + wm * 32 + i * 16 + frow;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int64_t n = n0 + wn * 32 + j * 16 + fg * 4;
+            if (n < N) mx = max(mx, store4<OUT_DT>(C, N, m, n, M, N, acc[i][j], sh, vec_out != 0));
+        }
+    }
+    if (AMAX) {
+        mx = wave_max_u32(mx);
+        if (lane == 0) atomicMax(amax_out, mx);
+    }
+}
+
+__global__ void fill_u32_kernel(uint32_t* p, uint32_t v) {
+    if (threadIdx.x == 0 && blockIdx.x == 0) *p = v;
+}
+
+template <int FA, int FB, int OUT_DT, bool AMAX>
+void launch_t(const uint8_t* A, const int32_t* ba, const uint8_t* B, const int32_t* bb, void* C,
+              int64_t M, int64_t N, int64_t K, uint32_t* amax, hipStream_t s) {
+    const int esz = OUT_DT == FP8_DT_BF16 ? 2 : 4;
+    const int vec_out = ((uintptr_t)C % (4 * esz) == 0) && (N % 4 == 0);
+    const bool fast = (K % kBK == 0) && ((uintptr_t)A % 16 == 0) && ((uintptr_t)B % 16 == 0) &&
+                      M <= INT32_MAX && N <= INT32_MAX && K <= INT32_MAX;
+    if (fast) {
+        const int tiles_m = (int)((M + kBM - 1) / kBM), tiles_n = (int)((N + kBN - 1) / kBN);
+        hipLaunchKernelGGL((gemm_nt_256<FA, FB, OUT_DT, AMAX>), dim3(tiles_m * tiles_n), dim3(kThreads), 0,
+                           s, A, B, ba, bb, C, (int)M, (int)N, (int)K, tiles_m, tiles_n, vec_out, amax);
+    } else {
+        const int64_t tiles_m = (M + kSBM - 1) / kSBM, tiles_n = (N + kSBN - 1) / kSBN;
+        hipLaunchKernelGGL((gemm_nt_small<FA, FB, OUT_DT, AMAX>), dim3((unsigned)(tiles_m * tiles_n)),
+                           dim3(kThreads), 0, s, A, B, ba, bb, C, M, N, K, tiles_n, vec_out, amax);
+    }
+}
+
+template <int FA, int FB>
+void dispatch_out(const uint8_t* A, const int32_t* ba, const uint8_t* B, const int32_t* bb, void* C,
+                  int out_dt, int64_t M, int64_t N, int64_t K, uint32_t* amax, hipStream_t s) {
+    if (out_dt == FP8_DT_BF16) {
+        if (amax) launch_t<FA, FB, FP8_DT_BF16, true>(A, ba, B, bb, C, M, N, K, amax, s);
+        else launch_t<FA, FB, FP8_DT_BF16, false>(A, ba, B, bb, C, M, N, K, amax, s);
+    } else {
+        if (amax) launch_t<FA, FB, FP8_DT_F32, true>(A, ba, B, bb, C, M, N, K, amax, s);
+        else launch_t<FA, FB, FP8_DT_F32, false>(A, ba, B, bb, C, M, N, K, amax, s);
+    }
+}
+
+}  // namespace
+
+int32_t launch_gemm_nt(const uint8_t* A, int fa, const int32_t* ba, const uint8_t* B, int fb,
+                       const int32_t* bb, void* C, int out_dt, int64_t M, int64_t N, int64_t K,
+                       uint32_t* amax_bits, hipStream_t s) {
+    if (amax_bits) hipLaunchKernelGGL(fill_u32_kernel, dim3(1), dim3(64), 0, s, amax_bits, 0u);
+    if (fa == FP8_E4M3 && fb == FP8_E4M3)
+        dispatch_out<FP8_E4M3, FP8_E4M3>(A, ba, B, bb, C, out_dt, M, N, K, amax_bits, s);
+    else if (fa == FP8_E5M2 && fb == FP8_E4M3)
+        dispatch_out<FP8_E5M2, FP8_E4M3>(A, ba, B, bb, C, out_dt, M, N, K, amax_bits, s);
+    else if (fa == FP8_E4M3 && fb == FP8_E5M2)
+        dispatch_out<FP8_E4M3, FP8_E5M2>(A, ba, B, bb, C, out_dt, M, N, K, amax_bits, s);
+    else
+        dispatch_out<FP8_E5M2, FP8_E5M2>(A, ba, B, bb, C, out_dt, M, N, K, amax_bits, s);
+    return hip_status();
+}
+
+}  // namespace fp8lin

@@ -1,0 +1,36 @@
+// Internal declarations shared by the translation units of libfp8lin.so.
+// Not part of the ABI: the public interface is include/fp8lin.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "fp8lin.h"
+
+namespace fp8lin {
+
+// Threads and block cap of the amax reduction: one fp32 partial per block.
+constexpr int kAmaxThreads = 256;
+constexpr int kAmaxMaxBlocks = 2048;
+
+int amax_blocks(int64_t n);
+
+int32_t launch_scale_bias(const void* x, int dt, int64_t n, int fmt, int32_t margin, int32_t* bias,
+                          uint32_t* amax_bits, uint32_t* flags, uint32_t* partials,
+                          hipStream_t s);
+int32_t launch_bias_from_amax(const uint32_t* amax_bits, int fmt, int32_t margin, int32_t* bias,
+                              uint32_t* flags, hipStream_t s);
+int32_t launch_cast(const void* x, int dt, int64_t rows, int64_t cols, int64_t ldx, int fmt,
+                    const int32_t* bias, uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT,
+                    hipStream_t s);
+
+// C[m, n] = 2^-(*ba + *bb) * sum_k A[m, k] * B[n, k]; A [M, K] (format fa),
+// B [N, K] (format fb), both dense; C [M, N] dense of type out_dt.
+int32_t launch_gemm_nt(const uint8_t* A, int fa, const int32_t* ba, const uint8_t* B, int fb,
+                       const int32_t* bb, void* C, int out_dt, int64_t M, int64_t N, int64_t K,
+                       uint32_t* amax_bits, hipStream_t s);
+
+inline int32_t hip_status() { return hipGetLastError() == hipSuccess ? FP8_OK : FP8_EHIP; }
+
+}  // namespace fp8lin

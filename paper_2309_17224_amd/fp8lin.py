@@ -1,0 +1,232 @@
+"""Thin ctypes binding of libfp8lin.so (include/fp8lin.h).
+
+Argument marshalling only: every function passes device pointers, sizes and
+the current HIP stream to the C entry point of the same name and raises
+Fp8Error on a non-zero status.  All arithmetic happens in the HIP kernels.
+PyTorch provides device memory and streams.  If the shared library has not
+been built the first call raises; nothing here falls back to another
+implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfp8lin.so")
+
+E4M3, E5M2 = 0, 1
+DT_BF16, DT_F32 = 0, 1
+FLAG_NONFINITE, FLAG_ZERO = 1, 2
+OK, EINVAL, ENOTSUP, EHIP = 0, 1, 2, 3
+
+# Every symbol declared in include/fp8lin.h.
+EXPORTS = (
+    "fp8_status_string", "fp8_abi_version", "fp8_scale_bias_ws_bytes", "fp8_scale_bias",
+    "fp8_bias_from_amax", "fp8_cast_e4", "fp8_cast_e5", "fp8_linear_fwd", "fp8_linear_bwd_dx",
+    "fp8_linear_bwd_dw", "ptq_quantise_weights",
+)
+
+
+class Fp8Error(RuntimeError):
+    def __init__(self, fn: str, status: int, msg: str):
+        super().__init__(f"{fn} failed with status {status}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2309_17224_amd.build` (hipcc, gfx950)")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        L.fp8_status_string.restype = ctypes.c_char_p
+        L.fp8_status_string.argtypes = [i32]
+        L.fp8_abi_version.restype = i32
+        L.fp8_abi_version.argtypes = []
+        L.fp8_scale_bias_ws_bytes.restype = sz
+        L.fp8_scale_bias_ws_bytes.argtypes = [i64]
+        L.fp8_scale_bias.restype = i32
+        L.fp8_scale_bias.argtypes = [vp, i32, i64, i32, i32, vp, vp, vp, vp, sz, vp]
+        L.fp8_bias_from_amax.restype = i32
+        L.fp8_bias_from_amax.argtypes = [vp, i32, i32, vp, vp, vp]
+        for name in ("fp8_cast_e4", "fp8_cast_e5"):
+            f = getattr(L, name)
+            f.restype = i32
+            f.argtypes = [vp, i32, i64, i64, i64, vp, vp, i64, vp, i64, vp]
+        for name in ("fp8_linear_fwd", "fp8_linear_bwd_dx"):
+            f = getattr(L, name)
+            f.restype = i32
+            f.argtypes = [vp, vp, vp, vp, vp, i32, i64, i64, i64, vp, vp]
+        L.fp8_linear_bwd_dw.restype = i32
+        L.fp8_linear_bwd_dw.argtypes = [vp, vp, vp, vp, vp, i32, i64, i64, i64, vp]
+        L.ptq_quantise_weights.restype = i32
+        L.ptq_quantise_weights.argtypes = [vp, i32, i64, i64, vp, vp, vp, vp, vp, sz, vp]
+        _lib = L
+    return _lib
+
+
+def _check(fn: str, status: int) -> None:
+    if status != OK:
+        raise Fp8Error(fn, status, lib().fp8_status_string(status).decode())
+
+
+def _p(t: torch.Tensor | None):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return DT_BF16
+    if t.dtype == torch.float32:
+        return DT_F32
+    raise TypeError(f"expected bfloat16 or float32, got {t.dtype}")
+
+
+def _ld(t: torch.Tensor) -> int:
+    """Row stride (elements) of a 2-D tensor whose rows are contiguous."""
+    if t.dim() != 2 or (t.stride(1) != 1 and t.size(1) > 1):
+        raise ValueError("expected a 2-D tensor with contiguous rows")
+    return t.stride(0) if t.size(0) > 1 else max(t.size(1), 1)
+
+
+def _i32(dev):
+    return torch.empty(1, dtype=torch.int32, device=dev)
+
+
+# ------------------------------------------------------------------ calls
+def fp8_scale_bias_ws_bytes(n: int) -> int:
+    return int(lib().fp8_scale_bias_ws_bytes(int(n)))
+
+
+def workspace(n: int, device) -> torch.Tensor:
+    return torch.empty(max(fp8_scale_bias_ws_bytes(n), 4), dtype=torch.uint8, device=device)
+
+
+def fp8_scale_bias(x: torch.Tensor, fmt: int, margin: int = 0, bias=None, amax_bits=None,
+                   flags=None, ws=None, stream=None):
+    """amax + Eq. 3 bias of a whole tensor.  Returns (bias, amax_bits, flags),
+    each a one-element device tensor (int32 / int32 holding uint32 bits)."""
+    if not x.is_contiguous():
+        raise ValueError("fp8_scale_bias needs a contiguous tensor")
+    dev = x.device
+    bias = _i32(dev) if bias is None else bias
+    amax_bits = _i32(dev) if amax_bits is None else amax_bits
+    flags = _i32(dev) if flags is None else flags
+    n = x.numel()
+    ws = workspace(n, dev) if ws is None else ws
+    st = lib().fp8_scale_bias(_p(x), _dt(x), n, fmt, margin, _p(bias), _p(amax_bits), _p(flags),
+                              _p(ws), ws.numel() * ws.element_size(), _stream(stream))
+    _check("fp8_scale_bias", st)
+    return bias, amax_bits, flags
+
+
+def fp8_bias_from_amax(amax_bits: torch.Tensor, fmt: int, margin: int = 0, bias=None, flags=None,
+                       stream=None):
+    dev = amax_bits.device
+    bias = _i32(dev) if bias is None else bias
+    flags = _i32(dev) if flags is None else flags
+    st = lib().fp8_bias_from_amax(_p(amax_bits), fmt, margin, _p(bias), _p(flags), _stream(stream))
+    _check("fp8_bias_from_amax", st)
+    return bias, flags
+
+
+def _cast(name: str, x: torch.Tensor, bias: torch.Tensor, q=None, qT=None, want_q=True,
+          want_qT=False, stream=None):
+    x2 = x if x.dim() == 2 else x.reshape(1, -1)
+    rows, cols = x2.shape
+    if want_q and q is None:
+        q = torch.empty((rows, cols), dtype=torch.uint8, device=x.device)
+    if want_qT and qT is None:
+        qT = torch.empty((cols, rows), dtype=torch.uint8, device=x.device)
+    st = getattr(lib(), name)(_p(x2), _dt(x2), rows, cols, _ld(x2), _p(bias),
+                              _p(q), _ld(q) if q is not None else 0,
+                              _p(qT), _ld(qT) if qT is not None else 0, _stream(stream))
+    _check(name, st)
+    return q, qT
+
+
+def fp8_cast_e4(x, bias, q=None, qT=None, want_q=True, want_qT=False, stream=None):
+    """Scale by 2^bias and cast to E4M3; returns (q, qT)."""
+    return _cast("fp8_cast_e4", x, bias, q, qT, want_q, want_qT, stream)
+
+
+def fp8_cast_e5(x, bias, q=None, qT=None, want_q=True, want_qT=False, stream=None):
+    """Scale by 2^bias and cast to E5M2; returns (q, qT)."""
+    return _cast("fp8_cast_e5", x, bias, q, qT, want_q, want_qT, stream)
+
+
+def _out(shape, out_dt, dev, out):
+    if out is not None:
+        return out
+    return torch.empty(shape, dtype=torch.bfloat16 if out_dt == DT_BF16 else torch.float32,
+                       device=dev)
+
+
+def _odt(out_dt: int, out) -> int:
+    return out_dt if out is None else _dt(out)
+
+
+def fp8_linear_fwd(x8, bx, w8t, bw, out_dt=DT_BF16, y=None, y_amax_bits=None, stream=None):
+    """Y [M,N] = 2^-(bx+bw) X8 [M,K] . W8T [N,K]^T."""
+    M, K = x8.shape
+    N = w8t.shape[0]
+    y = _out((M, N), out_dt, x8.device, y)
+    st = lib().fp8_linear_fwd(_p(x8), _p(bx), _p(w8t), _p(bw), _p(y), _odt(out_dt, y), M, N, K,
+                              _p(y_amax_bits), _stream(stream))
+    _check("fp8_linear_fwd", st)
+    return y
+
+
+def fp8_linear_bwd_dx(dy8, bg, w8, bw, out_dt=DT_BF16, dx=None, dx_amax_bits=None, stream=None):
+    """dX [M,K] = 2^-(bg+bw) dY8 [M,N] . W8 [K,N]^T."""
+    M, N = dy8.shape
+    K = w8.shape[0]
+    dx = _out((M, K), out_dt, dy8.device, dx)
+    st = lib().fp8_linear_bwd_dx(_p(dy8), _p(bg), _p(w8), _p(bw), _p(dx), _odt(out_dt, dx), M, N, K,
+                                 _p(dx_amax_bits), _stream(stream))
+    _check("fp8_linear_bwd_dx", st)
+    return dx
+
+
+def fp8_linear_bwd_dw(x8t, bx, dy8t, bg, out_dt=DT_F32, dw=None, stream=None):
+    """dW [K,N] = 2^-(bx+bg) X8T [K,M] . dY8T [N,M]^T."""
+    K, M = x8t.shape
+    N = dy8t.shape[0]
+    dw = _out((K, N), out_dt, x8t.device, dw)
+    st = lib().fp8_linear_bwd_dw(_p(x8t), _p(bx), _p(dy8t), _p(bg), _p(dw), _odt(out_dt, dw), M, N, K,
+                                 _stream(stream))
+    _check("fp8_linear_bwd_dw", st)
+    return dw
+
+
+def ptq_quantise_weights(w, want_w8=True, want_w8t=True, w8=None, w8t=None, bw=None, flags=None,
+                         ws=None, stream=None):
+    """Post-training quantisation of a [K, N] weight: returns (w8, w8t, bw, flags)."""
+    if not w.is_contiguous():
+        raise ValueError("ptq_quantise_weights needs a contiguous weight")
+    K, N = w.shape
+    dev = w.device
+    if want_w8 and w8 is None:
+        w8 = torch.empty((K, N), dtype=torch.uint8, device=dev)
+    if want_w8t and w8t is None:
+        w8t = torch.empty((N, K), dtype=torch.uint8, device=dev)
+    bw = _i32(dev) if bw is None else bw
+    flags = _i32(dev) if flags is None else flags
+    ws = workspace(K * N, dev) if ws is None else ws
+    st = lib().ptq_quantise_weights(_p(w), _dt(w), K, N, _p(w8), _p(w8t), _p(bw), _p(flags), _p(ws),
+                                    ws.numel() * ws.element_size(), _stream(stream))
+    _check("ptq_quantise_weights", st)
+    return w8, w8t, bw, flags

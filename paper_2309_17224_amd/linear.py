@@ -1,0 +1,273 @@
+"""The FP8 linear layer of the paper as a sequence of library calls.
+
+Training (Sec. 2, 2.2, 2.3, 3): three scaling biases per layer and call,
+  b_w = bias(W, E4)   W8, W8T = cast_E4(W * 2^b_w)     (after each weight update)
+  b_x = bias(X, E4)   X8, X8T = cast_E4(X * 2^b_x)
+  Y   = 2^-(b_x + b_w) X8 . W8                          (fp32 accumulate)
+  b_g = bias(dY, E5) - margin   dY8, dY8T = cast_E5(dY * 2^b_g)
+  dX  = 2^-(b_g + b_w) dY8 . W8^T
+  dW  = 2^-(b_x + b_g) X8^T . dY8
+The forward and grad-input matmuls also return the amax of their outputs
+(epilogue reduction), from which the next consumer's bias is taken without a
+second read of Y or dX (fp8_bias_from_amax).
+
+Inference (Sec. 3.1): W8T and b_w come once from ptq_quantise_weights; each
+call computes b_x and X8, then the forward matmul.
+
+Every buffer is allocated once, up front; a step launches kernels only.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import torch
+
+from . import fp8lin as F
+
+
+@dataclass
+class LinearBuffers:
+    M: int
+    K: int
+    N: int
+    device: torch.device
+    w8: torch.Tensor
+    w8t: torch.Tensor
+    x8: torch.Tensor
+    x8t: torch.Tensor
+    dy8: torch.Tensor
+    dy8t: torch.Tensor
+    y: torch.Tensor
+    dx: torch.Tensor
+    dw: torch.Tensor
+    scal: torch.Tensor      # int32 [16]: biases, amax bits, flags
+    ws: torch.Tensor
+
+    # views into scal
+    @property
+    def bw(self): return self.scal[0:1]
+    @property
+    def bx(self): return self.scal[1:2]
+    @property
+    def bg(self): return self.scal[2:3]
+    @property
+    def by(self): return self.scal[3:4]       # bias of Y for the next layer (E4)
+    @property
+    def bdx(self): return self.scal[4:5]      # bias of dX for the previous layer (E5)
+    @property
+    def amax_w(self): return self.scal[5:6]
+    @property
+    def amax_x(self): return self.scal[6:7]
+    @property
+    def amax_g(self): return self.scal[7:8]
+    @property
+    def amax_y(self): return self.scal[8:9]
+    @property
+    def amax_dx(self): return self.scal[9:10]
+    @property
+    def flags_w(self): return self.scal[10:11]
+    @property
+    def flags_x(self): return self.scal[11:12]
+    @property
+    def flags_g(self): return self.scal[12:13]
+    @property
+    def flags_y(self): return self.scal[13:14]
+    @property
+    def flags_dx(self): return self.scal[14:15]
+
+
+def alloc(M: int, K: int, N: int, device, y_dtype=torch.bfloat16, dx_dtype=torch.bfloat16,
+          dw_dtype=torch.float32, train: bool = True) -> LinearBuffers:
+    u8 = dict(dtype=torch.uint8, device=device)
+    e = torch.empty
+    nmax = max(M * K, K * N, M * N)
+    return LinearBuffers(
+        M, K, N, torch.device(device),
+        w8=e((K, N), **u8) if train else e((0, 0), **u8), w8t=e((N, K), **u8),
+        x8=e((M, K), **u8), x8t=e((K, M), **u8) if train else e((0, 0), **u8),
+        dy8=e((M, N), **u8) if train else e((0, 0), **u8),
+        dy8t=e((N, M), **u8) if train else e((0, 0), **u8),
+        y=e((M, N), dtype=y_dtype, device=device),
+        dx=e((M, K), dtype=dx_dtype, device=device) if train else e((0, 0), dtype=dx_dtype, device=device),
+        dw=e((K, N), dtype=dw_dtype, device=device) if train else e((0, 0), dtype=dw_dtype, device=device),
+        scal=torch.zeros(16, dtype=torch.int32, device=device),
+        ws=F.workspace(nmax, device),
+    )
+
+
+def quantise_weight(w: torch.Tensor, b: LinearBuffers) -> None:
+    """bias + cast of the weight: after every weight update (Sec. 3.2), or
+    once at checkpoint load (Sec. 3.1)."""
+    F.fp8_scale_bias(w, F.E4M3, 0, bias=b.bw, amax_bits=b.amax_w, flags=b.flags_w, ws=b.ws)
+    F.fp8_cast_e4(w, b.bw, q=b.w8, qT=b.w8t)
+
+
+def forward(x: torch.Tensor, b: LinearBuffers, keep_xt: bool = True) -> torch.Tensor:
+    F.fp8_scale_bias(x, F.E4M3, 0, bias=b.bx, amax_bits=b.amax_x, flags=b.flags_x, ws=b.ws)
+    F.fp8_cast_e4(x, b.bx, q=b.x8, qT=b.x8t if keep_xt else None, want_qT=keep_xt)
+    F.fp8_linear_fwd(b.x8, b.bx, b.w8t, b.bw, y=b.y, y_amax_bits=b.amax_y)
+    F.fp8_bias_from_amax(b.amax_y, F.E4M3, 0, bias=b.by, flags=b.flags_y)
+    return b.y
+
+
+def backward(dy: torch.Tensor, b: LinearBuffers, margin: int = 0):
+    F.fp8_scale_bias(dy, F.E5M2, margin, bias=b.bg, amax_bits=b.amax_g, flags=b.flags_g, ws=b.ws)
+    F.fp8_cast_e5(dy, b.bg, q=b.dy8, qT=b.dy8t)
+    F.fp8_linear_bwd_dx(b.dy8, b.bg, b.w8, b.bw, dx=b.dx, dx_amax_bits=b.amax_dx)
+    F.fp8_bias_from_amax(b.amax_dx, F.E5M2, margin, bias=b.bdx, flags=b.flags_dx)
+    F.fp8_linear_bwd_dw(b.x8t, b.bx, b.dy8t, b.bg, dw=b.dw)
+    return b.dx, b.dw
+
+
+def train_step(x: torch.Tensor, w: torch.Tensor, dy: torch.Tensor, b: LinearBuffers,
+               margin: int = 0):
+    """One fwd + bwd pass of one FP8 linear layer, weight cast included."""
+    quantise_weight(w, b)
+    y = forward(x, b)
+    dx, dw = backward(dy, b, margin)
+    return y, dx, dw
+
+
+def infer_step(x: torch.Tensor, b: LinearBuffers) -> torch.Tensor:
+    """PTQ inference call: activation bias + cast, then the forward matmul
+    with the weight quantised beforehand (quantise_weight / ptq)."""
+    F.fp8_scale_bias(x, F.E4M3, 0, bias=b.bx, amax_bits=b.amax_x, flags=b.flags_x, ws=b.ws)
+    F.fp8_cast_e4(x, b.bx, q=b.x8)
+    F.fp8_linear_fwd(b.x8, b.bx, b.w8t, b.bw, y=b.y)
+    return b.y
+
+
+# ---------------------------------------------------------------- workloads
+class Fp8Tensor:
+    """Device buffers of one high-precision tensor's FP8 form: codes, the
+    transposed codes, and [bias, amax bits, flags] as int32."""
+
+    def __init__(self, rows: int, cols: int, device, want_q=True, want_qT=True):
+        u8 = dict(dtype=torch.uint8, device=device)
+        self.q = torch.empty((rows, cols), **u8) if want_q else None
+        self.qT = torch.empty((cols, rows), **u8) if want_qT else None
+        self.scal = torch.zeros(3, dtype=torch.int32, device=device)
+
+    @property
+    def bias(self): return self.scal[0:1]
+    @property
+    def amax(self): return self.scal[1:2]
+    @property
+    def flags(self): return self.scal[2:3]
+
+
+class WorkloadStep:
+    """One pass of the FP8 path over all linear layers of a workload.
+
+    Training: every weight and every distinct activation / gradient tensor is
+    amax-scaled and cast once (an activation shared by several linears, such
+    as the input of gate and up projections, is cast once), then the forward,
+    grad-input and grad-weight matmuls of each linear run, the first two with
+    the epilogue amax and the bias of their outputs.  Inference: activations
+    are scaled and cast per call, weights once beforehand (PTQ).
+    ``calls`` lists (label, kind, flops_or_bytes, fn); running them in order
+    is one step.
+    """
+
+    def __init__(self, workload, tensors: dict, device, margin: int = 0):
+        self.w = workload
+        self.t = tensors
+        self.dev = torch.device(device)
+        self.margin = margin
+        lin = workload.linears
+        nmax = max(x.numel() for x in tensors.values())
+        self.ws = F.workspace(nmax, device)
+        self.q = {}
+        train = workload.train
+        for l in lin:
+            K, N, M = l.K, l.N, l.M
+            if l.w not in self.q:
+                self.q[l.w] = Fp8Tensor(K, N, device, want_q=train, want_qT=True)
+            if l.x not in self.q:
+                self.q[l.x] = Fp8Tensor(M, K, device, want_q=True, want_qT=train)
+            if train and l.dy not in self.q:
+                self.q[l.dy] = Fp8Tensor(M, N, device, want_q=True, want_qT=True)
+        self.out = {}
+        for l in lin:
+            o = dict(y=torch.empty((l.M, l.N), dtype=torch.bfloat16, device=device),
+                     y_scal=torch.zeros(3, dtype=torch.int32, device=device))
+            if train:
+                o.update(dx=torch.empty((l.M, l.K), dtype=torch.bfloat16, device=device),
+                         dw=torch.empty((l.K, l.N), dtype=torch.float32, device=device),
+                         dx_scal=torch.zeros(3, dtype=torch.int32, device=device))
+            self.out[l.name] = o
+        self.calls = self._build()
+
+    def _quant(self, name, fmt, margin):
+        x = self.t[name]
+        qt = self.q[name]
+        cast = F.fp8_cast_e4 if fmt == F.E4M3 else F.fp8_cast_e5
+        n = x.numel()
+        return [
+            (f"amax+bias {name}", "amax", 2 * n,
+             lambda: F.fp8_scale_bias(x, fmt, margin, bias=qt.bias, amax_bits=qt.amax,
+                                      flags=qt.flags, ws=self.ws)),
+            (f"cast {name}", "cast", 3 * n + (n if qt.qT is not None and qt.q is not None else 0),
+             lambda: cast(x, qt.bias, q=qt.q, qT=qt.qT, want_q=qt.q is not None,
+                          want_qT=qt.qT is not None)),
+        ]
+
+    def _build(self):
+        calls = []
+        lin = self.w.linears
+        done = set()
+        weights = [l.w for l in lin]
+        if self.w.train:
+            for name in dict.fromkeys(weights):
+                calls += self._quant(name, F.E4M3, 0)
+                done.add(name)
+        for l in lin:
+            if l.x not in done:
+                calls += self._quant(l.x, F.E4M3, 0)
+                done.add(l.x)
+        for l in lin:
+            xq, wq, o = self.q[l.x], self.q[l.w], self.out[l.name]
+            flop = 2 * l.M * l.N * l.K
+            calls.append((f"fwd {l.name}", "gemm_fwd", flop,
+                          lambda xq=xq, wq=wq, o=o: F.fp8_linear_fwd(
+                              xq.q, xq.bias, wq.qT, wq.bias, y=o["y"],
+                              y_amax_bits=o["y_scal"][1:2] if self.w.train else None)))
+            if self.w.train:
+                calls.append((f"bias y {l.name}", "bias", 0,
+                              lambda o=o: F.fp8_bias_from_amax(o["y_scal"][1:2], F.E4M3, 0,
+                                                               bias=o["y_scal"][0:1],
+                                                               flags=o["y_scal"][2:3])))
+        if self.w.train:
+            for l in lin:
+                if l.dy not in done:
+                    calls += self._quant(l.dy, F.E5M2, self.margin)
+                    done.add(l.dy)
+            for l in lin:
+                xq, wq, gq, o = self.q[l.x], self.q[l.w], self.q[l.dy], self.out[l.name]
+                flop = 2 * l.M * l.N * l.K
+                calls.append((f"dx {l.name}", "gemm_dx", flop,
+                              lambda wq=wq, gq=gq, o=o: F.fp8_linear_bwd_dx(
+                                  gq.q, gq.bias, wq.q, wq.bias, dx=o["dx"],
+                                  dx_amax_bits=o["dx_scal"][1:2])))
+                calls.append((f"bias dx {l.name}", "bias", 0,
+                              lambda o=o: F.fp8_bias_from_amax(o["dx_scal"][1:2], F.E5M2,
+                                                               self.margin, bias=o["dx_scal"][0:1],
+                                                               flags=o["dx_scal"][2:3])))
+                calls.append((f"dw {l.name}", "gemm_dw", flop,
+                              lambda xq=xq, gq=gq, o=o: F.fp8_linear_bwd_dw(
+                                  xq.qT, xq.bias, gq.qT, gq.bias, dw=o["dw"])))
+        return calls
+
+    def prepare_inference(self):
+        """PTQ: quantise every weight once (not part of the per-call step)."""
+        for name in dict.fromkeys(l.w for l in self.w.linears):
+            qt = self.q[name]
+            F.ptq_quantise_weights(self.t[name], want_w8=False, w8t=qt.qT, bw=qt.bias,
+                                   flags=qt.flags, ws=self.ws)
+
+    def run(self):
+        for _, _, _, fn in self.calls:
+            fn()
+
+    def gemm_flops(self) -> int:
+        return sum(v for _, kind, v, _ in self.calls if kind.startswith("gemm"))

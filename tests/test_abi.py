@@ -1,0 +1,106 @@
+"""The C ABI on the host (no GPU needed): the library loads, exports every
+function include/fp8lin.h declares, and rejects bad arguments before it would
+launch anything (status FP8_EINVAL, see the header's conventions)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2309_17224_amd import fp8lin as F
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fp8lin.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*([a-z_0-9]+)\s*\(", text, re.M)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(F.LIB_PATH):
+        from paper_2309_17224_amd import build
+        build.build()
+    return F.lib()
+
+
+def test_header_and_binding_agree():
+    assert declared_functions() == sorted(F.EXPORTS)
+
+
+def test_every_declared_symbol_is_exported(L):
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def test_status_strings(L):
+    assert L.fp8_status_string(0) == b"ok"
+    assert L.fp8_status_string(1) == b"invalid argument"
+    assert L.fp8_status_string(99) == b"unknown status"
+    assert L.fp8_abi_version() == 1
+
+
+def test_workspace_size(L):
+    assert L.fp8_scale_bias_ws_bytes(0) == 0
+    assert L.fp8_scale_bias_ws_bytes(1) == 4
+    assert L.fp8_scale_bias_ws_bytes(10 ** 9) == 4 * 2048
+
+
+FAKE = ctypes.c_void_p(0x100000)       # aligned, never dereferenced: rejected before launch
+ODD = ctypes.c_void_p(0x100001)
+NULL = None
+
+
+def test_scale_bias_rejects(L):
+    f = L.fp8_scale_bias
+    assert f(FAKE, 2, 10, 0, 0, FAKE, NULL, NULL, FAKE, 64, NULL) == F.EINVAL      # dtype
+    assert f(FAKE, 0, 10, 7, 0, FAKE, NULL, NULL, FAKE, 64, NULL) == F.EINVAL      # format
+    assert f(FAKE, 0, -1, 0, 0, FAKE, NULL, NULL, FAKE, 64, NULL) == F.EINVAL      # n < 0
+    assert f(NULL, 0, 10, 0, 0, FAKE, NULL, NULL, FAKE, 64, NULL) == F.EINVAL      # x
+    assert f(FAKE, 0, 10, 0, 0, NULL, NULL, NULL, FAKE, 64, NULL) == F.EINVAL      # bias
+    assert f(ODD, 0, 10, 0, 0, FAKE, NULL, NULL, FAKE, 64, NULL) == F.EINVAL       # alignment
+    assert f(FAKE, 0, 10, 0, 0, FAKE, NULL, NULL, NULL, 64, NULL) == F.EINVAL      # workspace
+    assert f(FAKE, 0, 10 ** 8, 0, 0, FAKE, NULL, NULL, FAKE, 4, NULL) == F.EINVAL  # too small
+    assert f(FAKE, 0, 10, 0, 1 << 20, FAKE, NULL, NULL, FAKE, 64, NULL) == F.EINVAL  # margin
+
+
+def test_cast_rejects(L):
+    for f in (L.fp8_cast_e4, L.fp8_cast_e5):
+        assert f(FAKE, 0, 4, 8, 8, FAKE, NULL, 8, NULL, 4, NULL) == F.EINVAL   # no output
+        assert f(FAKE, 0, 4, 8, 7, FAKE, FAKE, 8, NULL, 4, NULL) == F.EINVAL   # ldx < cols
+        assert f(FAKE, 0, 4, 8, 8, FAKE, FAKE, 7, NULL, 4, NULL) == F.EINVAL   # ldq < cols
+        assert f(FAKE, 0, 4, 8, 8, FAKE, NULL, 0, FAKE, 3, NULL) == F.EINVAL   # ldqT < rows
+        assert f(NULL, 0, 4, 8, 8, FAKE, FAKE, 8, NULL, 4, NULL) == F.EINVAL   # x
+        assert f(FAKE, 0, 4, 8, 8, NULL, FAKE, 8, NULL, 4, NULL) == F.EINVAL   # bias
+        assert f(FAKE, 5, 4, 8, 8, FAKE, FAKE, 8, NULL, 4, NULL) == F.EINVAL   # dtype
+        assert f(ODD, 0, 4, 8, 8, FAKE, FAKE, 8, NULL, 4, NULL) == F.EINVAL    # alignment
+        assert f(FAKE, 0, -4, 8, 8, FAKE, FAKE, 8, NULL, 4, NULL) == F.EINVAL  # rows < 0
+        assert f(NULL, 0, 0, 8, 8, NULL, NULL, 8, NULL, 4, NULL) == F.OK       # empty: no-op
+
+
+def test_gemm_rejects(L):
+    for f in (L.fp8_linear_fwd, L.fp8_linear_bwd_dx):
+        assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 3, 4, 4, 4, NULL, NULL) == F.EINVAL    # out dtype
+        assert f(NULL, FAKE, FAKE, FAKE, FAKE, 0, 4, 4, 4, NULL, NULL) == F.EINVAL    # operand
+        assert f(FAKE, NULL, FAKE, FAKE, FAKE, 0, 4, 4, 4, NULL, NULL) == F.EINVAL    # bias
+        assert f(FAKE, FAKE, FAKE, FAKE, NULL, 0, 4, 4, 4, NULL, NULL) == F.EINVAL    # output
+        assert f(FAKE, FAKE, FAKE, FAKE, ODD, 0, 4, 4, 4, NULL, NULL) == F.EINVAL     # alignment
+        assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 0, -1, 4, 4, NULL, NULL) == F.EINVAL   # M < 0
+        assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 0, 4, 4, 4, ODD, NULL) == F.EINVAL     # amax
+        assert f(NULL, NULL, NULL, NULL, NULL, 0, 0, 4, 4, NULL, NULL) == F.OK        # empty
+    f = L.fp8_linear_bwd_dw
+    assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 2, 4, 4, 4, NULL) == F.EINVAL
+    assert f(FAKE, FAKE, NULL, FAKE, FAKE, 0, 4, 4, 4, NULL) == F.EINVAL
+    assert f(NULL, NULL, NULL, NULL, NULL, 0, 4, 0, 4, NULL) == F.OK
+
+
+def test_ptq_and_bias_from_amax_reject(L):
+    assert L.ptq_quantise_weights(FAKE, 0, 4, 4, NULL, NULL, FAKE, NULL, FAKE, 64, NULL) == F.EINVAL
+    assert L.ptq_quantise_weights(FAKE, 0, 4, 4, FAKE, NULL, NULL, NULL, FAKE, 64, NULL) == F.EINVAL
+    assert L.ptq_quantise_weights(FAKE, 9, 4, 4, FAKE, NULL, FAKE, NULL, FAKE, 64, NULL) == F.EINVAL
+    assert L.fp8_bias_from_amax(NULL, 0, 0, FAKE, NULL, NULL) == F.EINVAL
+    assert L.fp8_bias_from_amax(FAKE, 3, 0, FAKE, NULL, NULL) == F.EINVAL
+    assert L.fp8_bias_from_amax(FAKE, 0, 0, ODD, NULL, NULL) == F.EINVAL

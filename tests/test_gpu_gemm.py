@@ -1,0 +1,133 @@
+"""GPU parity of the three FP8 matmuls (forward, grad-input, grad-weight)
+against the oracle's fp64-accumulated result (Sec. 2, 2.2; Eq. 2).
+
+Bar: rel_F = ||Y - Y_ref||_F / ||Y_ref||_F <= 1e-3 with Y_ref rounded to the
+same output type; bit-for-bit where every partial sum is exact in fp32.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2309_17224_amd import fp8lin as F
+from parity_util import REL_F_TOL, i32, np_bits, rel_f, u32
+
+pytestmark = pytest.mark.gpu
+
+ODT = {F.DT_BF16: torch.bfloat16, F.DT_F32: torch.float32}
+
+
+def rand_codes(shape, fmt, rng, orc):
+    """Random finite FP8 codes (uniform over codes, so all binades appear)."""
+    tab = orc.decode_table(fmt)
+    ok = np.nonzero(np.isfinite(tab))[0].astype(np.uint8)
+    return rng.choice(ok, size=shape)
+
+
+def run_nt(entry, A, fa, ba, B, fb, bb, out_dt, gpu, M, N, K, amax=False):
+    """Call one entry point on operands A [M,K], B [N,K] given in NT form."""
+    dev = gpu
+    ta = torch.from_numpy(np.ascontiguousarray(A)).to(dev)
+    tb = torch.from_numpy(np.ascontiguousarray(B)).to(dev)
+    pa = torch.tensor([ba], dtype=torch.int32, device=dev)
+    pb = torch.tensor([bb], dtype=torch.int32, device=dev)
+    am = torch.zeros(1, dtype=torch.int32, device=dev) if amax else None
+    if entry == "fwd":      # Y[M,N] = X8[M,K] . W8T[N,K]^T
+        out = F.fp8_linear_fwd(ta, pa, tb, pb, out_dt=out_dt, y_amax_bits=am)
+    elif entry == "dx":     # dX[M,K'] = dY8[M,N'] . W8[K',N']^T: here N' = K, K' = N
+        out = F.fp8_linear_bwd_dx(ta, pa, tb, pb, out_dt=out_dt, dx_amax_bits=am)
+    else:                   # dW[K',N'] = X8T[K',M'] . dY8T[N',M']^T: K' = M, M' = K
+        out = F.fp8_linear_bwd_dw(ta, pa, tb, pb, out_dt=out_dt)
+    torch.cuda.synchronize()
+    return np_bits(out), (u32(am) if amax else None)
+
+
+ENTRY_FMTS = {"fwd": (0, 0), "dx": (1, 0), "dw": (0, 1)}
+SHAPES = [(1, 1, 128), (16, 16, 128), (256, 256, 256), (300, 200, 384), (17, 129, 1000),
+          (255, 1, 17), (1, 255, 640), (129, 257, 128), (513, 300, 512), (64, 64, 0)]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "%dx%dx%d" % s)
+@pytest.mark.parametrize("entry", ["fwd", "dx", "dw"])
+@pytest.mark.parametrize("out_dt", [F.DT_BF16, F.DT_F32], ids=["bf16", "f32"])
+def test_gemm_random_codes(orc, gpu, shape, entry, out_dt):
+    M, N, K = shape
+    fa, fb = ENTRY_FMTS[entry]
+    rng = np.random.default_rng(M * 7 + N * 11 + K)
+    A = rand_codes((M, K), fa, rng, orc)
+    B = rand_codes((N, K), fb, rng, orc)
+    ba, bb = 9, 14 if fb == 1 else 6
+    got, _ = run_nt(entry, A, fa, ba, B, fb, bb, out_dt, gpu, M, N, K)
+    ref = orc.gemm_nt(A, fa, ba, B, fb, bb, out_dt=out_dt)
+    assert got.shape == (M, N)
+    assert rel_f(got, ref) <= REL_F_TOL
+
+
+@pytest.mark.parametrize("shape", [(16, 16, 128), (256, 512, 1024), (77, 300, 2048), (300, 77, 333)],
+                         ids=lambda s: "%dx%dx%d" % s)
+@pytest.mark.parametrize("entry", ["fwd", "dx", "dw"])
+def test_gemm_exact_small_integers_bit_for_bit(orc, gpu, shape, entry):
+    # Values in {0, +-1, ..., +-8} are exact in E4M3 and E5M2 and every
+    # partial sum stays an integer below 2^24: the fp32 result is unique.
+    M, N, K = shape
+    fa, fb = ENTRY_FMTS[entry]
+    vals = [0, 1, 2, 3, 4, 6, 8, -1, -2, -3, -4, -6, -8]
+    ca = np.array([orc.encode(fa, v) for v in vals], dtype=np.uint8)
+    cb = np.array([orc.encode(fb, v) for v in vals], dtype=np.uint8)
+    rng = np.random.default_rng(K)
+    ia = rng.integers(0, len(vals), (M, K))
+    ib = rng.integers(0, len(vals), (N, K))
+    got, _ = run_nt(entry, ca[ia], fa, 0, cb[ib], fb, 0, F.DT_F32, gpu, M, N, K)
+    v = np.array(vals, dtype=np.int64)
+    exact = (v[ia] @ v[ib].T).astype(np.float32)
+    assert np.array_equal(got, exact)
+    # the unscale is an exact power of two
+    got2, _ = run_nt(entry, ca[ia], fa, 3, cb[ib], fb, -1, F.DT_F32, gpu, M, N, K)
+    assert np.array_equal(got2, exact / 4)
+
+
+@pytest.mark.parametrize("out_dt", [F.DT_BF16, F.DT_F32], ids=["bf16", "f32"])
+def test_epilogue_amax(orc, gpu, out_dt):
+    M, N, K = 300, 520, 256
+    rng = np.random.default_rng(3)
+    A = rand_codes((M, K), 0, rng, orc)
+    B = rand_codes((N, K), 0, rng, orc)
+    got, amax = run_nt("fwd", A, 0, 10, B, 0, 10, out_dt, gpu, M, N, K, amax=True)
+    mag = np.abs(got.astype(np.uint16) & 0x7FFF).astype(np.uint32) << 16 if out_dt == F.DT_BF16 \
+        else got.view(np.uint32) & 0x7FFFFFFF
+    assert amax == int(mag.max())
+    # its bias equals the oracle's bias of the output tensor
+    ob, oa, ofl = orc.scale_bias(got, 0)
+    assert oa == amax
+    a = torch.tensor([amax], dtype=torch.int64).to(torch.int32).to(gpu)
+    b, fl = F.fp8_bias_from_amax(a, 0)
+    torch.cuda.synchronize()
+    assert (i32(b), u32(fl)) == (ob, ofl)
+    gotdx, amax_dx = run_nt("dx", rand_codes((M, K), 1, rng, orc), 1, 20, B, 0, 10, out_dt, gpu,
+                            M, N, K, amax=True)
+    _, oa2, _ = orc.scale_bias(gotdx, 1)
+    assert amax_dx == oa2
+
+
+def test_gemm_zero_sizes(gpu):
+    e = torch.empty((0, 128), dtype=torch.uint8, device=gpu)
+    w = torch.zeros((64, 128), dtype=torch.uint8, device=gpu)
+    b = torch.zeros(1, dtype=torch.int32, device=gpu)
+    y = F.fp8_linear_fwd(e, b, w, b)
+    assert y.shape == (0, 64)
+    # K == 0: zeros
+    x0 = torch.empty((5, 0), dtype=torch.uint8, device=gpu)
+    w0 = torch.empty((7, 0), dtype=torch.uint8, device=gpu)
+    y = F.fp8_linear_fwd(x0, b, w0, b, out_dt=F.DT_F32)
+    torch.cuda.synchronize()
+    assert y.shape == (5, 7) and float(y.abs().sum()) == 0.0
+
+
+def test_gemm_deterministic(orc, gpu):
+    rng = np.random.default_rng(12)
+    A = torch.from_numpy(rand_codes((512, 1024), 0, rng, orc)).to(gpu)
+    B = torch.from_numpy(rand_codes((768, 1024), 0, rng, orc)).to(gpu)
+    b = torch.tensor([5], dtype=torch.int32, device=gpu)
+    y1 = F.fp8_linear_fwd(A, b, B, b, out_dt=F.DT_F32)
+    y2 = F.fp8_linear_fwd(A, b, B, b, out_dt=F.DT_F32)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
