@@ -12,10 +12,13 @@
 //  * K advances 128 bytes at a time; both operand tiles (256 rows x 128 B)
 //    go HBM/L2 -> LDS with global_load_lds_dwordx4 (no VGPR staging) into a
 //    double buffer (2 x 64 KiB), so loads of step k+1 overlap the MFMAs of
-//    step k.
+//    step k; the copies are spread between MFMAs and one barrier per step
+//    orders both buffers (see the main loop).
 //  * LDS rows are 128 B; the 16-byte chunk index is XOR-swizzled with the row
-//    (chunk ^ (row & 7)) by choosing which global chunk each lane fetches, so
-//    the fragment reads (ds_read_b128) are free of bank conflicts.
+//    (chunk ^ ((row / 2) % 8)) by choosing which global chunk each lane
+//    fetches.  The LDS has 64 four-byte banks and serves 16 lanes of a
+//    ds_read_b128 per cycle; rows r and r+2 share banks, so this swizzle
+//    makes the 16 rows read together land on 16 distinct 16-byte bank groups.
 //  * A fragment of the 16x16x128 MFMA is 32 bytes per lane: row (lane % 16),
 //    32 consecutive k of group (lane / 16).  The matrix core pairs the same
 //    register bytes of both operands, so any k order that is the same for
@@ -78,6 +81,13 @@ template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
     static_assert(N >= 0 && N < 64, "vmcnt range");
     asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
+// The two 16-byte pieces of an MFMA operand fragment, as one 8-register vector.
+__device__ __forceinline__ v8i ld_frag(const uint8_t* p, int fo0, int fo1) {
+    const uint4 p0 = *(const uint4*)(p + fo0);
+    const uint4 p1 = *(const uint4*)(p + fo1);
+    return v8i{(int)p0.x, (int)p0.y, (int)p0.z, (int)p0.w, (int)p1.x, (int)p1.y, (int)p1.z, (int)p1.w};
 }
 
 // Contiguous tile ranges per XCD, then grouped row-major order inside.
@@ -153,36 +163,30 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_256(
     const int m0 = tm * kBM, n0 = tn * kBN;
 
     // Loader: wave w fills rows [64 w, 64 w + 64) of both tiles, 8 rows per
-    // instruction; lane -> row (lane / 8), physical chunk (lane % 8), which
-    // holds logical chunk (lane % 8) ^ (row % 8).
+    // instruction (src[0..7] for A, src[8..15] for B); lane -> row r =
+    // 64 w + 8 i + lane / 8 and physical chunk lane % 8, which holds logical
+    // chunk (lane % 8) ^ ((r / 2) % 8).
     const int lrow = lane >> 3;
-    const int lchunk = (lane & 7) ^ lrow;
-    const uint8_t* a_src[8];
-    const uint8_t* b_src[8];
+    const uint8_t* src[16];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-        const int ra = min(m0 + w * 64 + i * 8 + lrow, M - 1);
-        const int rb = min(n0 + w * 64 + i * 8 + lrow, N - 1);
-        a_src[i] = A + (int64_t)ra * K + lchunk * 16;
-        b_src[i] = B + (int64_t)rb * K + lchunk * 16;
+        const int r = w * 64 + i * 8 + lrow;
+        const int lchunk = (lane & 7) ^ ((r >> 1) & 7);
+        src[i] = A + (int64_t)min(m0 + r, M - 1) * K + lchunk * 16;
+        src[8 + i] = B + (int64_t)min(n0 + r, N - 1) * K + lchunk * 16;
     }
-
-    // LDS row address of this wave's first loader row (wave-uniform).
+    // LDS address of this wave's first loader row (wave-uniform); copy d of
+    // 16 goes to operand d / 8, row group d % 8.
     const uint32_t lds_w = __builtin_amdgcn_readfirstlane(lds_addr(smem) + w * 64 * kBK);
-    auto issue = [&](int stage, int k0) {
-        const uint32_t la = lds_w + stage * 2 * kTileBytes;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            lds_dma16(a_src[i] + k0, la + i * 8 * kBK);
-            lds_dma16(b_src[i] + k0, la + kTileBytes + i * 8 * kBK);
-        }
+    auto dma = [&](int d, int stage, int k0) {
+        lds_dma16(src[d] + k0, lds_w + stage * 2 * kTileBytes + (d >= 8 ? kTileBytes : 0) + (d & 7) * 8 * kBK);
     };
 
     const int wm = w >> 1, wn = w & 1;
     const int frow = lane & 15, fg = lane >> 4;
-    // byte offsets (within a tile) of this lane's two 16-byte fragment pieces
-    const int fo0 = frow * kBK + (((2 * fg) ^ (frow & 7)) << 4);
-    const int fo1 = frow * kBK + (((2 * fg + 1) ^ (frow & 7)) << 4);
+    // byte offsets (within a 16-row block) of this lane's two fragment pieces
+    const int fo0 = frow * kBK + (((2 * fg) ^ ((frow >> 1) & 7)) << 4);
+    const int fo1 = frow * kBK + (((2 * fg + 1) ^ ((frow >> 1) & 7)) << 4);
 
     v4f acc[8][8];
 #pragma unroll
@@ -190,35 +194,44 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_256(
 #pragma unroll
         for (int j = 0; j < 8; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
+    // Software pipeline, one barrier per k-step.  At the top of step kt every
+    // wave waits for its own copies of tile kt, then the barrier makes all of
+    // them visible and also guarantees that every wave has finished reading
+    // the other buffer (step kt-1), which the copies of tile kt+1 overwrite.
+    // Those 16 copies are issued between the first 16 MFMAs (issuing them in
+    // one burst stalls the wave's in-order issue behind the memory pipeline);
+    // B fragments are read 4 MFMAs ahead of use, the next A fragment two MFMAs
+    // into the current row.
     const int nk = K / kBK;
-    if (nk > 0) issue(0, 0);
+    if (nk > 0) {
+#pragma unroll
+        for (int d = 0; d < 16; ++d) dma(d, 0, 0);
+    }
     for (int kt = 0; kt < nk; ++kt) {
         const int st = kt & 1;
-        if (kt + 1 < nk) {
-            issue(st ^ 1, (kt + 1) * kBK);
-            wait_vmcnt<16>();
-        } else {
-            wait_vmcnt<0>();
-        }
+        const bool more = kt + 1 < nk;
+        const int k1 = (kt + 1) * kBK;
+        wait_vmcnt<0>();
         __syncthreads();
         const uint8_t* sa = smem + st * 2 * kTileBytes + wm * 128 * kBK;
         const uint8_t* sb = smem + st * 2 * kTileBytes + kTileBytes + wn * 128 * kBK;
-        v8i bf[8];
+        v8i bf[8], af[2];
+        af[0] = ld_frag(sa, fo0, fo1);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const uint4 p0 = *(const uint4*)(sb + j * 16 * kBK + fo0);
-            const uint4 p1 = *(const uint4*)(sb + j * 16 * kBK + fo1);
-            bf[j] = v8i{(int)p0.x, (int)p0.y, (int)p0.z, (int)p0.w, (int)p1.x, (int)p1.y, (int)p1.z, (int)p1.w};
-        }
+        for (int j = 0; j < 4; ++j) bf[j] = ld_frag(sb + j * 16 * kBK, fo0, fo1);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-            const uint4 p0 = *(const uint4*)(sa + i * 16 * kBK + fo0);
-            const uint4 p1 = *(const uint4*)(sa + i * 16 * kBK + fo1);
-            const v8i af = v8i{(int)p0.x, (int)p0.y, (int)p0.z, (int)p0.w, (int)p1.x, (int)p1.y, (int)p1.z, (int)p1.w};
 #pragma unroll
-            for (int j = 0; j < 8; ++j) acc[i][j] = mfma16<FB, FA>(bf[j], af, acc[i][j]);
+            for (int j = 0; j < 8; ++j) {
+                const int q = i * 8 + j;
+                if (i == 0 && j + 4 < 8) bf[j + 4] = ld_frag(sb + (j + 4) * 16 * kBK, fo0, fo1);
+                if (j == 2 && i + 1 < 8) af[(i + 1) & 1] = ld_frag(sa + (i + 1) * 16 * kBK, fo0, fo1);
+                if (q < 16 && more) dma(q, st ^ 1, k1);
+                acc[i][j] = mfma16<FB, FA>(bf[j], af[i & 1], acc[i][j]);
+                __builtin_amdgcn_sched_barrier(0);
+            }
         }
-        __syncthreads();
     }
 
     const int sh = -(*ba_p + *bb_p);
@@ -254,8 +267,8 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_small(
     const int lr = threadIdx.x >> 2, lq = threadIdx.x & 3;
     const int wm = w >> 1, wn = w & 1;
     const int frow = lane & 15, fg = lane >> 4;
-    const int fo0 = frow * kBK + (((2 * fg) ^ (frow & 7)) << 4);
-    const int fo1 = frow * kBK + (((2 * fg + 1) ^ (frow & 7)) << 4);
+    const int fo0 = frow * kBK + (((2 * fg) ^ ((frow >> 1) & 7)) << 4);
+    const int fo1 = frow * kBK + (((2 * fg + 1) ^ ((frow >> 1) & 7)) << 4);
 
     v4f acc[2][2];
 #pragma unroll
@@ -280,7 +293,7 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_small(
                     if (r < rmax && k < K) byte = src[r * K + k];
                     wv[t >> 2] |= byte << (8 * (t & 3));
                 }
-                *(uint4*)(dst + lr * kBK + ((c ^ (lr & 7)) << 4)) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+                *(uint4*)(dst + lr * kBK + ((c ^ ((lr >> 1) & 7)) << 4)) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
             }
         }
         __syncthreads();
