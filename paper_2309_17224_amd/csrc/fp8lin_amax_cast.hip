@@ -9,79 +9,35 @@
 // 16-bit max for bf16); pass 2 (one workgroup) reduces the partials and turns
 // the amax into the bias with integer arithmetic.
 //
-// cast: x * 2^b is formed exactly on the exponent field (no floating-point
-// multiply), then rounded to the FP8 grid with round-to-nearest-even in
-// integer arithmetic and clipped to the largest finite code.  The optional
-// transposed copy goes through a 128 x 64 byte LDS tile so that both outputs
-// are written with wide, coalesced stores.
+// cast: x * 2^b is formed with v_ldexp_f32, which is exact for every bf16 /
+// fp32 x (a power-of-two scale; results below the fp32 normal range are far
+// below half the smallest FP8 subnormal and become signed zeros either way),
+// clipped to +-max_num with v_med3_f32 (App. A: overflow clips to the
+// maximum; infinities included), and converted two at a time by
+// v_cvt_pk_fp8_f32 / v_cvt_pk_bf8_f32, which round to nearest even and keep
+// subnormals.  The converters encode NaN inputs as 0xFF / 0xFE and overflow
+// as NaN or infinity; the clip removes the overflow case and NaN inputs,
+// detected with a packed integer test, are re-encoded as 0x7F with their sign.
+// The transposed copy goes through a 128 x 128 byte LDS tile so that both
+// outputs leave as coalesced stores (whole 128-byte lines for the transpose).
 #include "fp8lin_internal.h"
 
 namespace fp8lin {
 namespace {
 
 // ---------------------------------------------------------------- formats
-// OCP FP8 (Table 7 rows "(b)").  kM: mantissa bits, kEmin: exponent of the
-// smallest normal, kMaxCode: code of the largest finite value.
+// OCP FP8 (Table 7 rows "(b)"): largest finite value 1.75 * 2^kMaxExp.
 template <int FMT> struct Fmt;
 template <> struct Fmt<FP8_E4M3> {
-    static constexpr int kM = 3, kEmin = -6, kMaxCode = 0x7E;
     static constexpr int kMaxExp = 8;  // max finite = 1.75 * 2^8 = 448
+    static constexpr float kMax = 448.0f;
 };
 template <> struct Fmt<FP8_E5M2> {
-    static constexpr int kM = 2, kEmin = -14, kMaxCode = 0x7B;
     static constexpr int kMaxExp = 15;  // max finite = 1.75 * 2^15 = 57344
+    static constexpr float kMax = 57344.0f;
 };
 
 constexpr int kBiasClamp = 512;  // beyond this every input saturates or flushes
-
-// Encode |value| = sig * 2^(E - (kSig - 1)), sig in [2^(kSig-1), 2^kSig), into the
-// magnitude bits of an FP8 code, rounding to nearest even and clipping.
-//   Ec = max(E, kEmin) is the exponent whose quantum 2^(Ec - kM) applies;
-//   n  = round(|value| / 2^(Ec - kM)); code = ((Ec - kEmin) << kM) + n.
-// A round-up that reaches 2^(kM+1) carries into the next binade by itself.
-template <int FMT, int kSig>
-__device__ __forceinline__ uint32_t encode_mag(uint32_t sig, int E) {
-    using F = Fmt<FMT>;
-    const int Ec = max(E, F::kEmin);
-    const int sh = min((kSig - 1 - F::kM) + (Ec - E), kSig + 2);
-    const uint32_t n = (sig + (1u << (sh - 1)) - 1u + ((sig >> sh) & 1u)) >> sh;
-    const int code = ((Ec - F::kEmin) << F::kM) + (int)n;
-    return (uint32_t)min(code, F::kMaxCode);
-}
-
-// bf16 bit pattern (low 16 bits of h) scaled by 2^b -> FP8 code.
-template <int FMT>
-__device__ __forceinline__ uint32_t enc_bf16(uint32_t h, int b) {
-    const uint32_t s = (h >> 8) & 0x80u;
-    const uint32_t a = h & 0x7FFFu;
-    const int e = (int)(a >> 7);
-    const uint32_t m = a & 0x7Fu;
-    const int p = 31 - __builtin_clz(m | 1u);          // top bit of a subnormal mantissa
-    const bool sub = (e == 0);
-    const int E = (sub ? p - 133 : e - 127) + b;
-    const uint32_t sig = sub ? (m << (7 - p)) : (m | 0x80u);
-    uint32_t c = encode_mag<FMT, 8>(sig, E);
-    c = (a == 0u) ? 0u : c;
-    c = (a >= 0x7F80u) ? ((a == 0x7F80u) ? (uint32_t)Fmt<FMT>::kMaxCode : 0x7Fu) : c;
-    return c | s;
-}
-
-// fp32 bit pattern scaled by 2^b -> FP8 code.
-template <int FMT>
-__device__ __forceinline__ uint32_t enc_f32(uint32_t u, int b) {
-    const uint32_t s = (u >> 24) & 0x80u;
-    const uint32_t a = u & 0x7FFFFFFFu;
-    const int e = (int)(a >> 23);
-    const uint32_t m = a & 0x7FFFFFu;
-    const int p = 31 - __builtin_clz(m | 1u);
-    const bool sub = (e == 0);
-    const int E = (sub ? p - 149 : e - 127) + b;
-    const uint32_t sig = sub ? (m << (23 - p)) : (m | 0x800000u);
-    uint32_t c = encode_mag<FMT, 24>(sig, E);
-    c = (a == 0u) ? 0u : c;
-    c = (a >= 0x7F800000u) ? ((a == 0x7F800000u) ? (uint32_t)Fmt<FMT>::kMaxCode : 0x7Fu) : c;
-    return c | s;
-}
 
 // Eq. 3 on the fp32 bit pattern of the amax: with amax = 1.f_a * 2^ea and
 // max_num = 1.75 * 2^eM, floor(log2(max_num / amax)) = eM - ea - [1.f_a > 1.75].
@@ -220,13 +176,76 @@ __global__ void bias_from_amax_kernel(const uint32_t* __restrict__ amax_bits, in
 }
 
 // ---------------------------------------------------------------- cast
-// Workgroup tile: 64 rows x 128 columns, 256 threads.  Lane l of wave w owns
-// rows r0 .. r0+3 (r0 = 16 w + 4 (l / 16)) and columns c0 .. c0+7
-// (c0 = 8 (l % 16)): each of its four row loads is one 16-byte (bf16) or two
-// 16-byte (fp32) accesses, and 16 lanes cover 256 contiguous bytes of a row.
-constexpr int kCastRows = 64, kCastCols = 128, kCastThreads = 256;
+// Two scaled, clipped values -> two codes in the low (HI = false) or high
+// half of `old`.
+template <int FMT, bool HI>
+__device__ __forceinline__ uint32_t cvt2(float a, float b, uint32_t old) {
+    if (FMT == FP8_E4M3) return __builtin_amdgcn_cvt_pk_fp8_f32(a, b, old, HI);
+    return __builtin_amdgcn_cvt_pk_bf8_f32(a, b, old, HI);
+}
 
-// Byte j of a 32-bit word.
+template <int FMT>
+__device__ __forceinline__ float scale_clip(float f, int b) {
+    return __builtin_amdgcn_fmed3f(ldexpf(f, b), -Fmt<FMT>::kMax, Fmt<FMT>::kMax);
+}
+
+// Four bf16 values (two packed words) -> four codes, before the NaN patch.
+template <int FMT>
+__device__ __forceinline__ uint32_t cast4_bf16(uint32_t w0, uint32_t w1, int b) {
+    const float f0 = __uint_as_float(w0 << 16), f1 = __uint_as_float(w0 & 0xFFFF0000u);
+    const float f2 = __uint_as_float(w1 << 16), f3 = __uint_as_float(w1 & 0xFFFF0000u);
+    const uint32_t c = cvt2<FMT, false>(scale_clip<FMT>(f0, b), scale_clip<FMT>(f1, b), 0u);
+    return cvt2<FMT, true>(scale_clip<FMT>(f2, b), scale_clip<FMT>(f3, b), c);
+}
+
+template <int FMT>
+__device__ __forceinline__ uint32_t cast4_f32(uint4 v, int b) {
+    const uint32_t c = cvt2<FMT, false>(scale_clip<FMT>(__uint_as_float(v.x), b), scale_clip<FMT>(__uint_as_float(v.y), b), 0u);
+    return cvt2<FMT, true>(scale_clip<FMT>(__uint_as_float(v.z), b), scale_clip<FMT>(__uint_as_float(v.w), b), c);
+}
+
+// Re-encode NaN inputs as 0x7F | sign.  hs[e] is input e as a bf16 pattern
+// or as the top half of an fp32 pattern with the low half folded into bit 0
+// (only the NaN test reads it).
+__device__ __forceinline__ uint32_t nan_patch(uint32_t c, const uint32_t hs[4]) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        if ((hs[e] & 0x7FFFu) > 0x7F80u) c = (c & ~(0xFFu << (8 * e))) | ((0x7Fu | ((hs[e] >> 8) & 0x80u)) << (8 * e));
+    return c;
+}
+
+// Packed test: does one of the four bf16 values in w0, w1 have a NaN pattern?
+__device__ __forceinline__ bool any_nan_bf16(uint32_t w0, uint32_t w1) {
+    return ((((w0 & 0x7FFF7FFFu) + 0x007F007Fu) | ((w1 & 0x7FFF7FFFu) + 0x007F007Fu)) & 0x80008000u) != 0u;
+}
+
+__device__ __forceinline__ uint32_t f32_key(uint32_t u) {  // fp32 pattern -> NaN-test key
+    return (u >> 16) | ((u & 0xFFFFu) ? 1u : 0u);
+}
+
+template <int DT, int FMT>
+__device__ __forceinline__ uint32_t cast1(const void* x, int64_t idx, int b) {
+    uint32_t key;
+    float f;
+    if (DT == FP8_DT_BF16) {
+        key = ((const uint16_t*)x)[idx];
+        f = __uint_as_float(key << 16);
+    } else {
+        const uint32_t u = ((const uint32_t*)x)[idx];
+        key = f32_key(u);
+        f = __uint_as_float(u);
+    }
+    uint32_t c = cvt2<FMT, false>(scale_clip<FMT>(f, b), 0.0f, 0u) & 0xFFu;
+    if ((key & 0x7FFFu) > 0x7F80u) c = 0x7Fu | ((key >> 8) & 0x80u);
+    return c;
+}
+
+// Workgroup tile: 128 rows x 128 columns, 256 threads.  Lane l of wave w owns
+// rows r0 .. r0+7 (r0 = 8 (4 w + l / 16)) and columns c0 .. c0+7
+// (c0 = 8 (l % 16)): each of its row loads is one 16-byte (bf16) or two
+// 16-byte (fp32) accesses, 16 lanes covering 256 (512) contiguous bytes.
+constexpr int kCastRows = 128, kCastCols = 128, kCastThreads = 256, kRpt = 8;
+
 __device__ __forceinline__ uint32_t byte_of(uint32_t w, int j) { return (w >> (8 * j)) & 0xFFu; }
 
 template <int DT, int FMT>
@@ -234,64 +253,59 @@ __global__ __launch_bounds__(kCastThreads) void cast_kernel(
     const void* __restrict__ x, int64_t rows, int64_t cols, int64_t ldx,
     const int32_t* __restrict__ bias_p, uint8_t* __restrict__ q, int64_t ldq,
     uint8_t* __restrict__ qT, int64_t ldqT, int64_t tiles_c, int vec_in, int vec_q, int vec_qT) {
-    // Transposed tile: 128 columns x 64 rows of codes; the 16-byte row chunk
-    // index is XOR-swizzled with the column block to spread LDS banks.
+    // Transposed tile: 128 columns x 128 rows of codes; within a column the
+    // 16-byte chunk index is XOR-swizzled with the column block.
     __shared__ __attribute__((aligned(16))) uint8_t tile[kCastCols * kCastRows];
 
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int chunk = lane & 15, g = lane >> 4;
     const int64_t tr = blockIdx.x / tiles_c, tc = blockIdx.x % tiles_c;
     const int64_t R0 = tr * kCastRows, C0 = tc * kCastCols;
-    const int lr = w * 16 + g * 4, lc = chunk * 8;  // local row / column of this lane
+    const int lr = (w * 4 + g) * kRpt, lc = chunk * 8;
     const int64_t r0 = R0 + lr, c0 = C0 + lc;
     const int b = max(-kBiasClamp, min(kBiasClamp, *bias_p));
 
-    uint32_t lo[4], hi[4];  // codes of columns c0..c0+3 and c0+4..c0+7, per row
-    const bool full = vec_in && (r0 + 4 <= rows) && (c0 + 8 <= cols);
+    uint32_t lo[kRpt], hi[kRpt];  // codes of columns c0..c0+3 and c0+4..c0+7, per row
+    const bool full = vec_in && (r0 + kRpt <= rows) && (c0 + 8 <= cols);
     if (full) {
         if (DT == FP8_DT_BF16) {
-            uint4 v[4];
+            uint4 v[kRpt];
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                v[i] = *(const uint4*)((const uint16_t*)x + (r0 + i) * ldx + c0);
+            for (int i = 0; i < kRpt; ++i) v[i] = *(const uint4*)((const uint16_t*)x + (r0 + i) * ldx + c0);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const uint32_t e0 = enc_bf16<FMT>(v[i].x & 0xFFFFu, b), e1 = enc_bf16<FMT>(v[i].x >> 16, b);
-                const uint32_t e2 = enc_bf16<FMT>(v[i].y & 0xFFFFu, b), e3 = enc_bf16<FMT>(v[i].y >> 16, b);
-                const uint32_t e4 = enc_bf16<FMT>(v[i].z & 0xFFFFu, b), e5 = enc_bf16<FMT>(v[i].z >> 16, b);
-                const uint32_t e6 = enc_bf16<FMT>(v[i].w & 0xFFFFu, b), e7 = enc_bf16<FMT>(v[i].w >> 16, b);
-                lo[i] = e0 | (e1 << 8) | (e2 << 16) | (e3 << 24);
-                hi[i] = e4 | (e5 << 8) | (e6 << 16) | (e7 << 24);
+            for (int i = 0; i < kRpt; ++i) {
+                lo[i] = cast4_bf16<FMT>(v[i].x, v[i].y, b);
+                hi[i] = cast4_bf16<FMT>(v[i].z, v[i].w, b);
+                if (__builtin_expect(any_nan_bf16(v[i].x, v[i].y) || any_nan_bf16(v[i].z, v[i].w), 0)) {
+                    const uint32_t h0[4] = {v[i].x & 0xFFFFu, v[i].x >> 16, v[i].y & 0xFFFFu, v[i].y >> 16};
+                    const uint32_t h1[4] = {v[i].z & 0xFFFFu, v[i].z >> 16, v[i].w & 0xFFFFu, v[i].w >> 16};
+                    lo[i] = nan_patch(lo[i], h0);
+                    hi[i] = nan_patch(hi[i], h1);
+                }
             }
         } else {
-            uint4 v[4][2];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
+            for (int i = 0; i < kRpt; ++i) {
                 const uint4* p = (const uint4*)((const uint32_t*)x + (r0 + i) * ldx + c0);
-                v[i][0] = p[0];
-                v[i][1] = p[1];
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                lo[i] = enc_f32<FMT>(v[i][0].x, b) | (enc_f32<FMT>(v[i][0].y, b) << 8) |
-                        (enc_f32<FMT>(v[i][0].z, b) << 16) | (enc_f32<FMT>(v[i][0].w, b) << 24);
-                hi[i] = enc_f32<FMT>(v[i][1].x, b) | (enc_f32<FMT>(v[i][1].y, b) << 8) |
-                        (enc_f32<FMT>(v[i][1].z, b) << 16) | (enc_f32<FMT>(v[i][1].w, b) << 24);
+                const uint4 a = p[0], bb = p[1];
+                lo[i] = cast4_f32<FMT>(a, b);
+                hi[i] = cast4_f32<FMT>(bb, b);
+                const uint32_t m = (a.x | a.y | a.z | a.w | bb.x | bb.y | bb.z | bb.w) & 0x7F800000u;
+                if (__builtin_expect(m == 0x7F800000u, 0)) {  // some exponent field may be all ones
+                    const uint32_t h0[4] = {f32_key(a.x), f32_key(a.y), f32_key(a.z), f32_key(a.w)};
+                    const uint32_t h1[4] = {f32_key(bb.x), f32_key(bb.y), f32_key(bb.z), f32_key(bb.w)};
+                    lo[i] = nan_patch(lo[i], h0);
+                    hi[i] = nan_patch(hi[i], h1);
+                }
             }
         }
     } else {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < kRpt; ++i) {
             uint32_t wlo = 0, whi = 0;
             for (int j = 0; j < 8; ++j) {
                 const int64_t r = r0 + i, c = c0 + j;
-                uint32_t code = 0;
-                if (r < rows && c < cols) {
-                    if (DT == FP8_DT_BF16)
-                        code = enc_bf16<FMT>(((const uint16_t*)x)[r * ldx + c], b);
-                    else
-                        code = enc_f32<FMT>(((const uint32_t*)x)[r * ldx + c], b);
-                }
+                const uint32_t code = (r < rows && c < cols) ? cast1<DT, FMT>(x, r * ldx + c, b) : 0u;
                 if (j < 4) wlo |= code << (8 * j); else whi |= code << (8 * (j - 4));
             }
             lo[i] = wlo;
@@ -302,39 +316,41 @@ __global__ __launch_bounds__(kCastThreads) void cast_kernel(
     if (q) {
         if (full && vec_q) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) *(uint2*)(q + (r0 + i) * ldq + c0) = make_uint2(lo[i], hi[i]);
+            for (int i = 0; i < kRpt; ++i) *(uint2*)(q + (r0 + i) * ldq + c0) = make_uint2(lo[i], hi[i]);
         } else {
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < kRpt; ++i)
                 for (int j = 0; j < 8; ++j) {
                     const int64_t r = r0 + i, c = c0 + j;
-                    if (r < rows && c < cols)
-                        q[r * ldq + c] = (uint8_t)byte_of(j < 4 ? lo[i] : hi[i], j & 3);
+                    if (r < rows && c < cols) q[r * ldq + c] = (uint8_t)byte_of(j < 4 ? lo[i] : hi[i], j & 3);
                 }
         }
     }
 
     if (qT) {
-        // Column j of this lane's 4x8 block, rows r0..r0+3, as one word.
+        // Column c0 + j of this lane's 8x8 block, rows r0..r0+7, as 8 bytes at
+        // row offset lr of transposed row lc + j.
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const uint32_t* src = j < 4 ? lo : hi;
             const int jj = j & 3;
-            const uint32_t col = byte_of(src[0], jj) | (byte_of(src[1], jj) << 8) |
-                                 (byte_of(src[2], jj) << 16) | (byte_of(src[3], jj) << 24);
+            const uint32_t w0 = byte_of(src[0], jj) | (byte_of(src[1], jj) << 8) | (byte_of(src[2], jj) << 16) |
+                                (byte_of(src[3], jj) << 24);
+            const uint32_t w1 = byte_of(src[4], jj) | (byte_of(src[5], jj) << 8) | (byte_of(src[6], jj) << 16) |
+                                (byte_of(src[7], jj) << 24);
             const int cl = lc + j;
-            const int off = cl * kCastRows + (((w ^ (cl >> 3)) & 3) << 4) + g * 4;
-            *(uint32_t*)(tile + off) = col;
+            const int off = cl * kCastRows + ((((lr >> 4) ^ (cl >> 3)) & 7) << 4) + (lr & 15);
+            *(uint2*)(tile + off) = make_uint2(w0, w1);
         }
         __syncthreads();
-        // 128 transposed rows x 4 chunks of 16 bytes = 512 chunks, two per thread.
+        // 128 transposed rows x 8 chunks of 16 bytes = 1024 chunks, four per thread.
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
+        for (int h = 0; h < 4; ++h) {
             const int idx = threadIdx.x + h * kCastThreads;
-            const int cl = idx >> 2, qq = idx & 3;
+            const int cl = idx >> 3, qq = idx & 7;
             const int64_t c = C0 + cl;
             const int64_t rr = R0 + qq * 16;
             if (c >= cols || rr >= rows) continue;
-            const uint4 v = *(const uint4*)(tile + cl * kCastRows + (((qq ^ (cl >> 3)) & 3) << 4));
+            const uint4 v = *(const uint4*)(tile + cl * kCastRows + (((qq ^ (cl >> 3)) & 7) << 4));
             uint8_t* dst = qT + c * ldqT + rr;
             if (vec_qT && rr + 16 <= rows) {
                 *(uint4*)dst = v;
