@@ -42,6 +42,9 @@ def parse():
                    help="seconds of oracle GEMM work in the CPU baseline sample")
     p.add_argument("--flush-mb", type=int, default=0,
                    help="write this many MB before every step (evicts the 256 MB MALL)")
+    p.add_argument("--copy-mb", type=int, default=0,
+                   help="only run a plain device-to-device copy of this many MB, --steps times "
+                        "(reference kernel for scaling hardware traffic counters), then exit")
     return p.parse_args()
 
 
@@ -103,7 +106,12 @@ def roofline(step, per_call):
     for kind, k in kinds.items():
         avg = k["time"] / k["launches"]
         per_launch = k["work"] / k["launches"]
-        if kind.startswith("gemm"):
+        if kind == "gemm_decode":
+            ach = per_launch / avg / 1e9 if avg > 0 else 0.0
+            table[kind] = dict(bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s",
+                               frac=ach / HBM_PEAK_GBS, avg_us=avg * 1e6, per_launch=per_launch,
+                               total_ms=k["time"] / steps * 1e3)
+        elif kind.startswith("gemm"):
             ach = per_launch / avg / 1e12 if avg > 0 else 0.0
             table[kind] = dict(bound="mfma", achieved=ach, peak=FP8_PEAK_TFLOPS, unit="TFLOP/s",
                                frac=ach / FP8_PEAK_TFLOPS, avg_us=avg * 1e6, per_launch=per_launch,
@@ -192,6 +200,15 @@ def main():
     from paper_2309_17224_amd import workloads as wl
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a GPU")
+    if args.copy_mb:
+        nbytes = args.copy_mb << 20
+        src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_per_launch": nbytes, "launches": args.steps}))
+        return
     fp8lin.lib()  # fails loudly when the HIP library is missing
     w = wl.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")

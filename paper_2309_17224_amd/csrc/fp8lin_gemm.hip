@@ -30,6 +30,7 @@
 //    XCDs; the remap gives each XCD a contiguous range of tiles, walked in
 //    groups of 8 tile-rows, so tiles sharing operand panels meet in the same
 //    L2.
+// Decode kernel (M <= 32): weight-streaming split-K, see below.
 // Fallback kernel (any K or alignment): 64 x 64 tiles, byte loads with
 // bounds checks and zero fill, same MFMA and epilogue.
 #include "fp8lin_internal.h"
@@ -331,6 +332,111 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_small(
     }
 }
 
+
+// ------------------------------------------------------------ decode kernel
+// M <= 32 (token-by-token inference): the product is bound by streaming B
+// (the FP8 weight, N x K bytes) from HBM once.  A workgroup of 8 waves owns
+// 64 output columns; wave w takes a contiguous slice of the K range, reads
+// its operand fragments straight from global memory into registers (two
+// steps in flight), and the 8 partial 16x64 (or 32x64) sums are added in LDS
+// in a fixed order, so the result does not depend on timing.
+
+__device__ __forceinline__ v8i ld_frag_g(const uint8_t* p) {
+    const uint4 p0 = *(const uint4*)p;
+    const uint4 p1 = *(const uint4*)(p + 16);
+    return v8i{(int)p0.x, (int)p0.y, (int)p0.z, (int)p0.w, (int)p1.x, (int)p1.y, (int)p1.z, (int)p1.w};
+}
+
+// NB: 16-column blocks per workgroup; kDecWaves: waves splitting the K range.
+template <int FA, int FB, int OUT_DT, bool AMAX, int MB, int NB, int kDecWaves>
+__global__ __launch_bounds__(kDecWaves * 64) void gemm_nt_decode(
+    const uint8_t* __restrict__ A, const uint8_t* __restrict__ B, const int32_t* __restrict__ ba_p,
+    const int32_t* __restrict__ bb_p, void* __restrict__ C, int M, int N, int K, int vec_out,
+    uint32_t* __restrict__ amax_out) {
+    __shared__ __attribute__((aligned(16))) float red[kDecWaves][MB][NB][64][4];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int n0 = blockIdx.x * NB * 16;
+    const int frow = lane & 15, fg = lane >> 4;
+    // fragment sources: row (lane % 16) of each 16-row block, 32 bytes at
+    // k-offset 32 (lane / 16) of every 128-byte step
+    const uint8_t* pa[MB];
+    const uint8_t* pb[NB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) pa[mb] = A + (int64_t)min(mb * 16 + frow, M - 1) * K + fg * 32;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) pb[j] = B + (int64_t)min(n0 + j * 16 + frow, N - 1) * K + fg * 32;
+    const int nkc = K / kBK;
+    const int c0 = (int)((int64_t)nkc * w / kDecWaves), c1 = (int)((int64_t)nkc * (w + 1) / kDecWaves);
+
+    v4f acc[MB][NB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int j = 0; j < NB; ++j) acc[mb][j] = v4f{0.f, 0.f, 0.f, 0.f};
+
+    // three k-steps in flight
+    v8i xa[3][MB], wb[3][NB];
+    auto load = [&](int slot, int c) {
+        const int64_t k0 = (int64_t)c * kBK;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) xa[slot][mb] = ld_frag_g(pa[mb] + k0);
+#pragma unroll
+        for (int j = 0; j < NB; ++j) wb[slot][j] = ld_frag_g(pb[j] + k0);
+    };
+    auto step = [&](int slot) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int j = 0; j < NB; ++j) acc[mb][j] = mfma16<FB, FA>(wb[slot][j], xa[slot][mb], acc[mb][j]);
+    };
+    if (c0 < c1) load(0, c0);
+    if (c0 + 1 < c1) load(1, c0 + 1);
+    for (int c = c0; c < c1; c += 3) {
+        if (c + 2 < c1) load(2, c + 2);
+        step(0);
+        if (c + 1 < c1) {
+            if (c + 3 < c1) load(0, c + 3);
+            step(1);
+        }
+        if (c + 2 < c1) {
+            if (c + 4 < c1) load(1, c + 4);
+            step(2);
+        }
+    }
+
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int j = 0; j < NB; ++j) *(v4f*)red[w][mb][j][lane] = acc[mb][j];
+    __syncthreads();
+    const int sh = -(*ba_p + *bb_p);
+    uint32_t mx = 0;
+    for (int slot = threadIdx.x; slot < MB * NB * 64; slot += kDecWaves * 64) {
+        const int mb = slot / (NB * 64), j = (slot / 64) % NB, l = slot & 63;
+        v4f sum = *(const v4f*)red[0][mb][j][l];
+#pragma unroll
+        for (int ww = 1; ww < kDecWaves; ++ww) sum += *(const v4f*)red[ww][mb][j][l];
+        const int64_t m = mb * 16 + (l & 15);
+        const int64_t n = n0 + j * 16 + (l >> 4) * 4;
+        if (n < N) mx = max(mx, store4<OUT_DT>(C, N, m, n, M, N, sum, sh, vec_out != 0));
+    }
+    if (AMAX) {
+        mx = wave_max_u32(mx);
+        if (lane == 0) atomicMax(amax_out, mx);
+    }
+}
+
+template <int FA, int FB, int OUT_DT, bool AMAX, int MB>
+void launch_decode(const uint8_t* A, const int32_t* ba, const uint8_t* B, const int32_t* bb, void* C,
+                   int M, int N, int K, int vec_out, uint32_t* amax, hipStream_t s) {
+    // 32 output columns per workgroup of 4 waves, each wave a quarter of the
+    // K range (the best of 1-8 column blocks x 4-16 waves on the Llama-2-70B
+    // decode shapes)
+    const int nblk = (N + 31) / 32;
+    hipLaunchKernelGGL((gemm_nt_decode<FA, FB, OUT_DT, AMAX, MB, 2, 4>), dim3(nblk), dim3(4 * 64), 0, s, A, B, ba,
+                       bb, C, M, N, K, vec_out, amax);
+}
+
 __global__ void fill_u32_kernel(uint32_t* p, uint32_t v) {
     if (threadIdx.x == 0 && blockIdx.x == 0) *p = v;
 }
@@ -342,7 +448,10 @@ void launch_t(const uint8_t* A, const int32_t* ba, const uint8_t* B, const int32
     const int vec_out = ((uintptr_t)C % (4 * esz) == 0) && (N % 4 == 0);
     const bool fast = (K % kBK == 0) && ((uintptr_t)A % 16 == 0) && ((uintptr_t)B % 16 == 0) &&
                       M <= INT32_MAX && N <= INT32_MAX && K <= INT32_MAX;
-    if (fast) {
+    if (fast && M <= 32) {
+        if (M <= 16) launch_decode<FA, FB, OUT_DT, AMAX, 1>(A, ba, B, bb, C, (int)M, (int)N, (int)K, vec_out, amax, s);
+        else launch_decode<FA, FB, OUT_DT, AMAX, 2>(A, ba, B, bb, C, (int)M, (int)N, (int)K, vec_out, amax, s);
+    } else if (fast) {
         const int tiles_m = (int)((M + kBM - 1) / kBM), tiles_n = (int)((N + kBN - 1) / kBN);
         hipLaunchKernelGGL((gemm_nt_256<FA, FB, OUT_DT, AMAX>), dim3(tiles_m * tiles_n), dim3(kThreads), 0,
                            s, A, B, ba, bb, C, (int)M, (int)N, (int)K, tiles_m, tiles_n, vec_out, amax);

@@ -228,7 +228,12 @@ class WorkloadStep:
         for l in lin:
             xq, wq, o = self.q[l.x], self.q[l.w], self.out[l.name]
             flop = 2 * l.M * l.N * l.K
-            calls.append((f"fwd {l.name}", "gemm_fwd", flop,
+            # M <= 32 runs the weight-streaming kernel: its work is counted in
+            # bytes (weight + activations + bf16 output), it is HBM-bound
+            kind, work = "gemm_fwd", flop
+            if l.M <= 32:
+                kind, work = "gemm_decode", l.N * l.K + l.M * l.K + 2 * l.M * l.N
+            calls.append((f"fwd {l.name}", kind, work,
                           lambda xq=xq, wq=wq, o=o: F.fp8_linear_fwd(
                               xq.q, xq.bias, wq.qT, wq.bias, y=o["y"],
                               y_amax_bits=o["y_scal"][1:2] if self.w.train else None)))
@@ -270,4 +275,4 @@ class WorkloadStep:
             fn()
 
     def gemm_flops(self) -> int:
-        return sum(v for _, kind, v, _ in self.calls if kind.startswith("gemm"))
+        return sum(2 * l.M * l.N * l.K * (3 if self.w.train else 1) for l in self.w.linears)

@@ -168,3 +168,29 @@ def test_gemm_deterministic(orc, gpu):
     y2 = F.fp8_linear_fwd(A, b, B, b, out_dt=F.DT_F32)
     torch.cuda.synchronize()
     assert torch.equal(y1, y2)
+
+
+# Decode shapes (M <= 32 routes to the weight-streaming kernel; 33 does not).
+DECODE = [(1, 64, 128), (2, 1000, 1024), (15, 65, 896), (16, 4096, 8192), (17, 130, 384),
+          (31, 192, 2048), (32, 1, 128), (33, 100, 256), (16, 63, 28672)]
+
+
+@pytest.mark.parametrize("shape", DECODE, ids=lambda s: "%dx%dx%d" % s)
+@pytest.mark.parametrize("out_dt", [F.DT_BF16, F.DT_F32], ids=["bf16", "f32"])
+def test_gemm_decode_shapes(orc, gpu, shape, out_dt):
+    M, N, K = shape
+    rng = np.random.default_rng(M * 131 + N + K)
+    A, ba = scaled_normal_codes((M, K), 0, rng, orc)
+    B, bb = scaled_normal_codes((N, K), 0, rng, orc)
+    got, amax = run_nt("fwd", A, 0, ba, B, 0, bb, out_dt, gpu, M, N, K, amax=True)
+    ref = orc.gemm_nt(A, 0, ba, B, 0, bb, out_dt=out_dt)
+    assert rel_f(got, ref) <= REL_F_TOL
+    mag = (got.astype(np.uint32) & 0x7FFF) << 16 if out_dt == F.DT_BF16 else got.view(np.uint32) & 0x7FFFFFFF
+    assert amax == int(mag.max())
+    # exact small integers: bit for bit
+    vals = [0, 1, 2, 3, -1, -2, -4]
+    c = np.array([orc.encode(0, v) for v in vals], dtype=np.uint8)
+    ia, ib = rng.integers(0, len(vals), (M, K)), rng.integers(0, len(vals), (N, K))
+    got, _ = run_nt("fwd", c[ia], 0, 0, c[ib], 0, 0, F.DT_F32, gpu, M, N, K)
+    v = np.array(vals, dtype=np.int64)
+    assert np.array_equal(got, (v[ia] @ v[ib].T).astype(np.float32))
