@@ -131,6 +131,26 @@ def roofline(step, per_call):
     return roof, table
 
 
+def measured_traffic(workload: str, kind: str):
+    """HBM bytes per launch of `kind` from the hardware-counter runs stored in
+    profiles/ (FETCH_SIZE and WRITE_SIZE scaled by a plain copy kernel), or
+    None when there is no measurement for this workload or the kernel sources
+    changed since it was taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    h = hashlib.sha256()
+    for src in ("fp8lin_gemm.hip", "fp8lin_amax_cast.hip"):
+        with open(os.path.join(ROOT, "paper_2309_17224_amd", "csrc", src), "rb") as f:
+            h.update(f.read())
+    if rec.get("kernel_sources_sha256") != h.hexdigest():
+        return None
+    return rec.get("bytes_per_launch", {}).get(kind)
+
+
 def cpu_baseline(w, cpu_tensors, budget_s):
     """The oracle, as it is, on a bounded sample of one step: amax, bias and
     cast on the full tensors, the matmuls on sampled rows, extrapolated
@@ -227,6 +247,7 @@ def main():
     flops = step.gemm_flops()
     value = flops / step_s / 1e12
     roof, table = roofline(step, per_call)
+    roof["traffic"] = measured_traffic(w.name, roof["kernel"])
     for kind, d in sorted(table.items()):
         log(f"[bench] {kind:9s} " + " ".join(f"{k}={v:.4g}" if isinstance(v, float) else f"{k}={v}"
                                              for k, v in d.items()))
