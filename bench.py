@@ -7,6 +7,10 @@ cast, forward matmul with epilogue amax, gradient bias and cast (E5), grad-input
 matmul with epilogue amax, grad-weight matmul.  Inputs are synthetic, seeded,
 already resident in HBM when timing starts.
 
+Timed steps replay one HIP graph that holds the whole step (--launch eager
+issues one host call per library call instead); a separate eager pass brackets
+every call with HIP events for the per-kernel table.
+
 Prints one JSON line:
   value      = 6*M*N*K per linear (fwd + bwd matmul FLOPs) / step time, TFLOP/s
   roofline   = the dominant kernel against its roofline, timed with HIP events
@@ -42,6 +46,9 @@ def parse():
                    help="seconds of oracle GEMM work in the CPU baseline sample")
     p.add_argument("--flush-mb", type=int, default=0,
                    help="write this many MB before every step (evicts the 256 MB MALL)")
+    p.add_argument("--launch", choices=("graph", "eager"), default="graph",
+                   help="timed steps: replays of one HIP graph holding the whole step, or "
+                        "one host call per library call")
     p.add_argument("--copy-mb", type=int, default=0,
                    help="only run a plain device-to-device copy of this many MB, --steps times "
                         "(reference kernel for scaling hardware traffic counters), then exit")
@@ -89,6 +96,30 @@ def time_steps(step, steps, warmup, flush=None):
                 for s in range(steps)]
     flush_s = sum(a.elapsed_time(b) * 1e-3 for a, b in fl_ev) if flush is not None else 0.0
     return wall, per_call, flush_s
+
+
+def time_graph(step, steps, warmup, flush=None):
+    """Wall time of `steps` replays of the captured step (HIP graph)."""
+    import torch
+    step.capture()
+    for _ in range(warmup):
+        if flush is not None:
+            flush.add_(1)
+        step.replay()
+    torch.cuda.synchronize()
+    fl_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+             for _ in range(steps)]
+    t0 = time.perf_counter()
+    for s in range(steps):
+        if flush is not None:
+            fl_ev[s][0].record()
+            flush.add_(1)
+            fl_ev[s][1].record()
+        step.replay()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    flush_s = sum(a.elapsed_time(b) * 1e-3 for a, b in fl_ev) if flush is not None else 0.0
+    return wall, flush_s
 
 
 def roofline(step, per_call):
@@ -242,8 +273,13 @@ def main():
     if args.flush_mb:
         flush = torch.zeros(args.flush_mb * (1 << 20) // 4, dtype=torch.float32, device=dev)
     log(f"[bench] {w.name}: {len(step.calls)} calls per step; warmup {args.warmup}, steps {args.steps}")
+    # eager pass: every call bracketed by HIP events on its stream (roofline table)
     wall, per_call, flush_s = time_steps(step, args.steps, args.warmup, flush)
-    step_s = (wall - flush_s) / args.steps
+    eager_step_s = (wall - flush_s) / args.steps
+    step_s = eager_step_s
+    if args.launch == "graph":
+        gwall, gflush = time_graph(step, args.steps, args.warmup, flush)
+        step_s = (gwall - gflush) / args.steps
     flops = step.gemm_flops()
     value = flops / step_s / 1e12
     roof, table = roofline(step, per_call)
@@ -254,13 +290,16 @@ def main():
     out = {
         "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_s * 1e3, 4),
+        "eager_ms_per_step": round(eager_step_s * 1e3, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "fp8",
         "data": "synthetic",
         "config": {"workload": w.name, "description": w.description,
                    "linears": [dict(name=l.name, M=l.M, K=l.K, N=l.N) for l in w.linears],
                    "mode": "train fwd+bwd" if w.train else "PTQ inference fwd",
                    "accumulate": "fp32", "outputs": "Y,dX bf16; dW fp32",
-                   "margin": args.margin, "mall_flush_mb": args.flush_mb},
+                   "margin": args.margin, "mall_flush_mb": args.flush_mb,
+                   "launch": "one HIP graph replay per step" if args.launch == "graph"
+                   else "one host call per library call"},
         "frac_of_fp8_peak": round(value / FP8_PEAK_TFLOPS, 4),
         "roofline": roof,
         "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv) for kk, vv in d.items()}

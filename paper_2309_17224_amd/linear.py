@@ -274,5 +274,22 @@ class WorkloadStep:
         for _, _, _, fn in self.calls:
             fn()
 
+    def capture(self):
+        """Record one step (every call, in order) into a HIP graph, so that
+        replay() launches the whole step with one host call.  The library
+        launches only kernels (no memset or copy nodes) on the current stream,
+        and every buffer is allocated beforehand, so replays recompute the
+        step from the current contents of the input tensors."""
+        torch.cuda.synchronize(self.dev)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            self.run()
+        torch.cuda.synchronize(self.dev)
+        self.graph = g
+        return g
+
+    def replay(self):
+        self.graph.replay()
+
     def gemm_flops(self) -> int:
         return sum(2 * l.M * l.N * l.K * (3 if self.w.train else 1) for l in self.w.linears)
