@@ -41,7 +41,9 @@
  *    largest finite FP8 value, infinities included, clip to it with their
  *    sign (App. A); NaN becomes 0x7F with the input's sign bit.
  *  - Matmul accumulation is fp32 (MFMA); the unscale 2^-(b_a + b_b) is applied
- *    to the fp32 sum, which is then rounded once to the output type.
+ *    to the fp32 sum, which is then rounded once to the output type (to
+ *    nearest, ties to even).  An output is NaN only when an operand holds a
+ *    NaN code; its NaN encoding is unspecified.
  *  - Thread safety: calls hold no state and may be issued from any thread.
  */
 #ifndef FP8LIN_H

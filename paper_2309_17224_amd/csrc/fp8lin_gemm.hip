@@ -61,19 +61,6 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
     return v;
 }
 
-// Direct HBM/L2 -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4):
-// lane i's 16 bytes land at lds_row + 16 i.  lds_row must be the same for the
-// whole wave.  The instruction is issued from inline assembly so that the
-// compiler does not treat every later LDS read as dependent on it (it cannot
-// tell the two halves of the double buffer apart and would wait for the
-// prefetch before each read); completion is tracked with wait_vmcnt below.
-__device__ __forceinline__ void lds_dma16(const uint8_t* g, uint32_t lds_row) {
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
-                 :
-                 : "s"(lds_row), "v"(g)
-                 : "memory");
-}
-
 // 32-bit LDS address of a pointer into a __shared__ array.
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
     return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
@@ -161,9 +148,13 @@ __device__ __forceinline__ uint32_t store4(void* C, int64_t ldc, int64_t m, int6
 constexpr int kBM = 256, kBN = 256, kBK = 128, kThreads = 256;
 constexpr int kTileBytes = kBM * kBK;  // one operand tile, 32 KiB
 
-// Copy of 16 bytes per lane into LDS with a wave-uniform 64-bit base in
-// SGPRs and a 32-bit per-lane offset (the "saddr" form): the address needs no
-// per-copy 64-bit vector add.
+// Direct L2 -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4, the
+// form with a wave-uniform 64-bit base in SGPRs and a 32-bit lane offset):
+// lane i's 16 bytes land at lds_row + 16 i; lds_row must be wave-uniform.
+// The instruction is issued from inline assembly so that the compiler does
+// not treat every later LDS read as dependent on it (it cannot tell the two
+// halves of the double buffer apart and would wait for the prefetch before
+// each read); completion is tracked with wait_vmcnt.
 __device__ __forceinline__ void lds_dma16_s(const uint8_t* sbase, uint32_t voff, uint32_t lds_row) {
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
                  :
@@ -443,11 +434,12 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_small(
 
 // ------------------------------------------------------------ decode kernel
 // M <= 32 (token-by-token inference): the product is bound by streaming B
-// (the FP8 weight, N x K bytes) from HBM once.  A workgroup of 8 waves owns
-// 64 output columns; wave w takes a contiguous slice of the K range, reads
-// its operand fragments straight from global memory into registers (two
-// steps in flight), and the 8 partial 16x64 (or 32x64) sums are added in LDS
-// in a fixed order, so the result does not depend on timing.
+// (the FP8 weight, N x K bytes) from HBM once.  A workgroup of kDecWaves
+// waves owns NB 16-column blocks; wave w takes a contiguous slice of the K
+// range, reads its operand fragments straight from global memory into
+// registers (three 128-byte k-steps in flight), and the partial sums of the
+// waves are added in LDS in a fixed order, so the result does not depend on
+// timing.
 
 __device__ __forceinline__ v8i ld_frag_g(const uint8_t* p) {
     const uint4 p0 = *(const uint4*)p;
