@@ -46,6 +46,10 @@ def parse():
                    help="seconds of oracle GEMM work in the CPU baseline sample")
     p.add_argument("--flush-mb", type=int, default=0,
                    help="write this many MB before every step (evicts the 256 MB MALL)")
+    p.add_argument("--quant", choices=("predicted", "twopass", "separate"), default="predicted",
+                   help="bias + cast of X, W, dY: one fp8_quantise call predicting each bias from "
+                        "the previous step (identical bits; one read of an unchanged tensor), "
+                        "fp8_quantise without prediction, or fp8_scale_bias + fp8_cast")
     p.add_argument("--launch", choices=("graph", "eager"), default="graph",
                    help="timed steps: replays of one HIP graph holding the whole step, or "
                         "one host call per library call")
@@ -147,7 +151,7 @@ def roofline(step, per_call):
             table[kind] = dict(bound="mfma", achieved=ach, peak=FP8_PEAK_TFLOPS, unit="TFLOP/s",
                                frac=ach / FP8_PEAK_TFLOPS, avg_us=avg * 1e6, per_launch=per_launch,
                                total_ms=k["time"] / steps * 1e3)
-        elif kind in ("amax", "cast"):
+        elif kind in ("amax", "cast", "quantise"):
             ach = per_launch / avg / 1e9 if avg > 0 else 0.0
             table[kind] = dict(bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s",
                                frac=ach / HBM_PEAK_GBS, avg_us=avg * 1e6, per_launch=per_launch,
@@ -266,7 +270,7 @@ def main():
     cpu = make_inputs(w)
     tens = {k: v.to(dev) for k, v in cpu.items()}
     torch.cuda.synchronize()
-    step = L.WorkloadStep(w, tens, dev, margin=args.margin)
+    step = L.WorkloadStep(w, tens, dev, margin=args.margin, quant=args.quant)
     if not w.train:
         step.prepare_inference()
     flush = None
@@ -297,7 +301,7 @@ def main():
                    "linears": [dict(name=l.name, M=l.M, K=l.K, N=l.N) for l in w.linears],
                    "mode": "train fwd+bwd" if w.train else "PTQ inference fwd",
                    "accumulate": "fp32", "outputs": "Y,dX bf16; dW fp32",
-                   "margin": args.margin, "mall_flush_mb": args.flush_mb,
+                   "margin": args.margin, "mall_flush_mb": args.flush_mb, "quant": args.quant,
                    "launch": "one HIP graph replay per step" if args.launch == "graph"
                    else "one host call per library call"},
         "frac_of_fp8_peak": round(value / FP8_PEAK_TFLOPS, 4),

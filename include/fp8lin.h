@@ -141,6 +141,33 @@ int32_t fp8_cast_e5(const void *x, int32_t dt, int64_t rows, int64_t cols, int64
                     void *stream);
 
 /*
+ * fp8_quantise -- amax, Eq. 3 bias and scale+cast of one whole tensor in one
+ * call (Sec. 2.3 Eq. 3, Sec. 2.1 Eq. 1): the same outputs, bit for bit, as
+ * fp8_scale_bias over the rows x cols elements followed by fp8_cast_e4 (fmt
+ * FP8_E4M3) or fp8_cast_e5 (FP8_E5M2).
+ * Computing the bias needs the amax of the whole tensor before any element
+ * can be cast, which costs a second pass over the tensor (Sec. 3).  A
+ * predicted bias removes that pass when the prediction is right: the tensor
+ * is read once, cast with the prediction while its amax is taken, and only if
+ * the exact bias differs from the prediction are the codes written again
+ * with the exact bias.  Biases of the same tensor change little from one step
+ * to the next (Sec. 3), so the previous step's bias is a good prediction.
+ * x, dt, rows, cols, ldx, q, ldq, qT, ldqT: as fp8_cast_e4 (strides allowed).
+ * fmt, margin: as fp8_scale_bias.
+ * bias_pred: in, optional, one int32 (device): the predicted bias; may be the
+ *            same word as bias.  NULL: two passes (amax, then the cast).
+ * bias, amax_bits, flags: out, as fp8_scale_bias (amax_bits, flags optional).
+ * ws:        device workspace of at least fp8_quantise_ws_bytes(rows, cols)
+ *            bytes, 4-byte aligned; scratch, distinct for concurrent calls.
+ * rows == 0 or cols == 0 gives amax 0, bias 0 and FP8_FLAG_ZERO, no codes.
+ */
+size_t fp8_quantise_ws_bytes(int64_t rows, int64_t cols);
+int32_t fp8_quantise(const void *x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx,
+                     int32_t fmt, int32_t margin, const int32_t *bias_pred, int32_t *bias,
+                     uint32_t *amax_bits, uint32_t *flags, uint8_t *q, int64_t ldq,
+                     uint8_t *qT, int64_t ldqT, void *ws, size_t ws_bytes, void *stream);
+
+/*
  * fp8_linear_fwd -- forward FP8 matmul with unscale (Sec. 2, Eq. 2):
  *   Y[m, n] = 2^-(bx + bw) * sum_k X8[m, k] * W8[k, n]
  * x8:  [M, K] E4M3 codes (dense), bias *bx.

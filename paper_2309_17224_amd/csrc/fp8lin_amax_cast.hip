@@ -248,30 +248,39 @@ constexpr int kCastRows = 128, kCastCols = 128, kCastThreads = 256, kRpt = 8;
 
 __device__ __forceinline__ uint32_t byte_of(uint32_t w, int j) { return (w >> (8 * j)) & 0xFFu; }
 
-template <int DT, int FMT>
-__global__ __launch_bounds__(kCastThreads) void cast_kernel(
-    const void* __restrict__ x, int64_t rows, int64_t cols, int64_t ldx,
-    const int32_t* __restrict__ bias_p, uint8_t* __restrict__ q, int64_t ldq,
-    uint8_t* __restrict__ qT, int64_t ldqT, int64_t tiles_c, int vec_in, int vec_q, int vec_qT) {
-    // Transposed tile: 128 columns x 128 rows of codes; within a column the
-    // 16-byte chunk index is XOR-swizzled with the column block.
-    __shared__ __attribute__((aligned(16))) uint8_t tile[kCastCols * kCastRows];
-
+// One 128 x 128 tile (tile row tr, tile column tc) of the cast with bias b:
+// codes to q (if given) and transposed codes to qT (if given).  With MAX, the
+// largest magnitude pattern of the tile's elements (bf16: 15 bits, fp32: 31
+// bits; 0 past the edges) is returned, valid in every thread after a block
+// reduction by the caller.  Every thread of the block must call it (it
+// synchronises through the LDS tile), and it leaves the LDS tile free for
+// the next call.
+template <int DT, int FMT, bool MAX>
+__device__ __forceinline__ uint32_t cast_tile(const void* __restrict__ x, int64_t rows, int64_t cols,
+                                              int64_t ldx, int b, uint8_t* __restrict__ q, int64_t ldq,
+                                              uint8_t* __restrict__ qT, int64_t ldqT, int64_t tr,
+                                              int64_t tc, int vec_in, int vec_q, int vec_qT,
+                                              uint8_t* __restrict__ tile) {
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int chunk = lane & 15, g = lane >> 4;
-    const int64_t tr = blockIdx.x / tiles_c, tc = blockIdx.x % tiles_c;
     const int64_t R0 = tr * kCastRows, C0 = tc * kCastCols;
     const int lr = (w * 4 + g) * kRpt, lc = chunk * 8;
     const int64_t r0 = R0 + lr, c0 = C0 + lc;
-    const int b = max(-kBiasClamp, min(kBiasClamp, *bias_p));
 
     uint32_t lo[kRpt], hi[kRpt];  // codes of columns c0..c0+3 and c0+4..c0+7, per row
+    uint32_t mag = 0;
     const bool full = vec_in && (r0 + kRpt <= rows) && (c0 + 8 <= cols);
     if (full) {
         if (DT == FP8_DT_BF16) {
             uint4 v[kRpt];
 #pragma unroll
             for (int i = 0; i < kRpt; ++i) v[i] = *(const uint4*)((const uint16_t*)x + (r0 + i) * ldx + c0);
+            if (MAX) {
+                us2 mm = {0, 0};
+#pragma unroll
+                for (int i = 0; i < kRpt; ++i) mm = fold_bf16(mm, v[i]);
+                mag = max((uint32_t)mm.x, (uint32_t)mm.y);
+            }
 #pragma unroll
             for (int i = 0; i < kRpt; ++i) {
                 lo[i] = cast4_bf16<FMT>(v[i].x, v[i].y, b);
@@ -288,6 +297,7 @@ __global__ __launch_bounds__(kCastThreads) void cast_kernel(
             for (int i = 0; i < kRpt; ++i) {
                 const uint4* p = (const uint4*)((const uint32_t*)x + (r0 + i) * ldx + c0);
                 const uint4 a = p[0], bb = p[1];
+                if (MAX) mag = fold_f32(fold_f32(mag, a), bb);
                 lo[i] = cast4_f32<FMT>(a, b);
                 hi[i] = cast4_f32<FMT>(bb, b);
                 const uint32_t m = (a.x | a.y | a.z | a.w | bb.x | bb.y | bb.z | bb.w) & 0x7F800000u;
@@ -305,7 +315,11 @@ __global__ __launch_bounds__(kCastThreads) void cast_kernel(
             uint32_t wlo = 0, whi = 0;
             for (int j = 0; j < 8; ++j) {
                 const int64_t r = r0 + i, c = c0 + j;
-                const uint32_t code = (r < rows && c < cols) ? cast1<DT, FMT>(x, r * ldx + c, b) : 0u;
+                uint32_t code = 0u;
+                if (r < rows && c < cols) {
+                    code = cast1<DT, FMT>(x, r * ldx + c, b);
+                    if (MAX) mag = max(mag, elem_mag<DT>(x, r * ldx + c));
+                }
                 if (j < 4) wlo |= code << (8 * j); else whi |= code << (8 * (j - 4));
             }
             lo[i] = wlo;
@@ -328,7 +342,8 @@ __global__ __launch_bounds__(kCastThreads) void cast_kernel(
 
     if (qT) {
         // Column c0 + j of this lane's 8x8 block, rows r0..r0+7, as 8 bytes at
-        // row offset lr of transposed row lc + j.
+        // row offset lr of transposed row lc + j; 16-byte chunks of a
+        // transposed row are XOR-swizzled with the column block.
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const uint32_t* src = j < 4 ? lo : hi;
@@ -359,7 +374,81 @@ __global__ __launch_bounds__(kCastThreads) void cast_kernel(
                 for (int t = 0; t < 16 && rr + t < rows; ++t) dst[t] = (uint8_t)byte_of(wv[t >> 2], t & 3);
             }
         }
+        __syncthreads();  // the tile may be rewritten by the next call
     }
+    return mag;
+}
+
+__device__ __forceinline__ int clamp_bias(int32_t b) { return max(-kBiasClamp, min(kBiasClamp, b)); }
+
+template <int DT, int FMT>
+__global__ __launch_bounds__(kCastThreads) void cast_kernel(
+    const void* __restrict__ x, int64_t rows, int64_t cols, int64_t ldx,
+    const int32_t* __restrict__ bias_p, uint8_t* __restrict__ q, int64_t ldq,
+    uint8_t* __restrict__ qT, int64_t ldqT, int64_t tiles_c, int vec_in, int vec_q, int vec_qT) {
+    __shared__ __attribute__((aligned(16))) uint8_t tile[kCastCols * kCastRows];
+    const int b = clamp_bias(*bias_p);
+    cast_tile<DT, FMT, false>(x, rows, cols, ldx, b, q, ldq, qT, ldqT, blockIdx.x / tiles_c,
+                              blockIdx.x % tiles_c, vec_in, vec_q, vec_qT, tile);
+}
+
+// ------------------------------------------------- quantise: amax + bias + cast
+// Pass 1 (quant_pass1_kernel), one workgroup per tile: the largest magnitude
+// pattern of the tile goes to parts[tile]; with CAST the tile is also cast with
+// the predicted bias (clamped), which block 0 records in *used.
+// Pass 2 (quant_pass2_kernel): every workgroup reduces parts[] and evaluates
+// Eq. 3; block 0 writes bias, amax and flags.  If pass 1 did not cast, or cast
+// with a bias other than the exact one, the workgroups recast all tiles
+// (grid-stride) with the exact bias; otherwise the codes of pass 1 are already
+// those of the exact bias and nothing more is written.
+template <int DT, int FMT, bool CAST>
+__global__ __launch_bounds__(kCastThreads) void quant_pass1_kernel(
+    const void* __restrict__ x, int64_t rows, int64_t cols, int64_t ldx,
+    const int32_t* __restrict__ bias_pred, int32_t* __restrict__ used, uint32_t* __restrict__ parts,
+    uint8_t* __restrict__ q, int64_t ldq, uint8_t* __restrict__ qT, int64_t ldqT, int64_t tiles_c,
+    int vec_in, int vec_q, int vec_qT) {
+    __shared__ __attribute__((aligned(16))) uint8_t tile[kCastCols * kCastRows];
+    __shared__ uint32_t red[kCastThreads / 64];
+    int b = 0;
+    if (CAST) {
+        b = clamp_bias(*bias_pred);
+        if (blockIdx.x == 0 && threadIdx.x == 0) *used = b;
+    }
+    const uint32_t m = cast_tile<DT, FMT, true>(x, rows, cols, ldx, b, CAST ? q : nullptr, ldq,
+                                                CAST ? qT : nullptr, ldqT, blockIdx.x / tiles_c,
+                                                blockIdx.x % tiles_c, vec_in, vec_q, vec_qT, tile);
+    const uint32_t bm = block_max(m, red);
+    if (threadIdx.x == 0) parts[blockIdx.x] = bm;
+}
+
+template <int DT, int FMT>
+__global__ __launch_bounds__(kCastThreads) void quant_pass2_kernel(
+    const void* __restrict__ x, int64_t rows, int64_t cols, int64_t ldx,
+    const uint32_t* __restrict__ parts, int nparts, const int32_t* __restrict__ used, int have_used,
+    int32_t margin, int32_t* __restrict__ bias, uint32_t* __restrict__ amax_bits,
+    uint32_t* __restrict__ flags, uint8_t* __restrict__ q, int64_t ldq, uint8_t* __restrict__ qT,
+    int64_t ldqT, int64_t tiles_c, int vec_in, int vec_q, int vec_qT) {
+    __shared__ __attribute__((aligned(16))) uint8_t tile[kCastCols * kCastRows];
+    __shared__ uint32_t red[kCastThreads / 64];
+    __shared__ uint32_t amax_s;
+    uint32_t m = 0;
+    for (int i = threadIdx.x; i < nparts; i += kCastThreads) m = max(m, parts[i]);
+    m = block_max(m, red);
+    if (threadIdx.x == 0) amax_s = m;
+    __syncthreads();
+    const uint32_t a32 = DT == FP8_DT_BF16 ? (amax_s << 16) : amax_s;
+    uint32_t fl;
+    const int32_t bx = bias_of<FMT>(a32, margin, &fl);
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        *bias = bx;
+        if (amax_bits) *amax_bits = a32;
+        if (flags) *flags = fl;
+    }
+    const int b = clamp_bias(bx);
+    if (have_used && *used == b) return;  // pass 1 already wrote these codes
+    for (int64_t t = blockIdx.x; t < nparts; t += gridDim.x)
+        cast_tile<DT, FMT, false>(x, rows, cols, ldx, b, q, ldq, qT, ldqT, t / tiles_c, t % tiles_c,
+                                  vec_in, vec_q, vec_qT, tile);
 }
 
 template <int DT, int FMT>
@@ -373,6 +462,36 @@ void launch_cast_t(const void* x, int64_t rows, int64_t cols, int64_t ldx, const
     const int vec_qT = qT && ((uintptr_t)qT % 16 == 0) && (ldqT % 16 == 0);
     hipLaunchKernelGGL((cast_kernel<DT, FMT>), dim3((unsigned)(tiles_r * tiles_c)), dim3(kCastThreads), 0,
                        s, x, rows, cols, ldx, bias, q, ldq, qT, ldqT, tiles_c, vec_in, vec_q, vec_qT);
+}
+
+constexpr int kQuantPass2MaxBlocks = 1024;
+
+template <int DT, int FMT>
+void launch_quantise_t(const void* x, int64_t rows, int64_t cols, int64_t ldx, int32_t margin,
+                       const int32_t* bias_pred, int32_t* bias, uint32_t* amax_bits, uint32_t* flags,
+                       uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT, uint32_t* ws,
+                       hipStream_t s) {
+    const int64_t tiles_r = (rows + kCastRows - 1) / kCastRows;
+    const int64_t tiles_c = (cols + kCastCols - 1) / kCastCols;
+    const int64_t ntiles = tiles_r * tiles_c;
+    const int esz = DT == FP8_DT_BF16 ? 2 : 4;
+    const int vec_in = ((uintptr_t)x % 16 == 0) && ((ldx * esz) % 16 == 0);
+    const int vec_q = q && ((uintptr_t)q % 8 == 0) && (ldq % 8 == 0);
+    const int vec_qT = qT && ((uintptr_t)qT % 16 == 0) && (ldqT % 16 == 0);
+    int32_t* used = (int32_t*)ws;
+    uint32_t* parts = ws + 1;
+    if (bias_pred)
+        hipLaunchKernelGGL((quant_pass1_kernel<DT, FMT, true>), dim3((unsigned)ntiles), dim3(kCastThreads), 0, s,
+                           x, rows, cols, ldx, bias_pred, used, parts, q, ldq, qT, ldqT, tiles_c, vec_in,
+                           vec_q, vec_qT);
+    else
+        hipLaunchKernelGGL((quant_pass1_kernel<DT, FMT, false>), dim3((unsigned)ntiles), dim3(kCastThreads), 0, s,
+                           x, rows, cols, ldx, bias_pred, used, parts, q, ldq, qT, ldqT, tiles_c, vec_in,
+                           vec_q, vec_qT);
+    const int nb2 = (int)(ntiles < kQuantPass2MaxBlocks ? ntiles : kQuantPass2MaxBlocks);
+    hipLaunchKernelGGL((quant_pass2_kernel<DT, FMT>), dim3(nb2), dim3(kCastThreads), 0, s, x, rows, cols, ldx,
+                       parts, (int)ntiles, used, bias_pred ? 1 : 0, margin, bias, amax_bits, flags, q, ldq,
+                       qT, ldqT, tiles_c, vec_in, vec_q, vec_qT);
 }
 
 }  // namespace
@@ -425,6 +544,26 @@ int32_t launch_cast(const void* x, int dt, int64_t rows, int64_t cols, int64_t l
         launch_cast_t<FP8_DT_F32, FP8_E4M3>(x, rows, cols, ldx, bias, q, ldq, qT, ldqT, s);
     else
         launch_cast_t<FP8_DT_F32, FP8_E5M2>(x, rows, cols, ldx, bias, q, ldq, qT, ldqT, s);
+    return hip_status();
+}
+
+int64_t quantise_ws_words(int64_t rows, int64_t cols) {
+    const int64_t tiles = ((rows + kCastRows - 1) / kCastRows) * ((cols + kCastCols - 1) / kCastCols);
+    return 1 + tiles;
+}
+
+int32_t launch_quantise(const void* x, int dt, int64_t rows, int64_t cols, int64_t ldx, int fmt,
+                        int32_t margin, const int32_t* bias_pred, int32_t* bias, uint32_t* amax_bits,
+                        uint32_t* flags, uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT,
+                        uint32_t* ws, hipStream_t s) {
+    if (dt == FP8_DT_BF16 && fmt == FP8_E4M3)
+        launch_quantise_t<FP8_DT_BF16, FP8_E4M3>(x, rows, cols, ldx, margin, bias_pred, bias, amax_bits, flags, q, ldq, qT, ldqT, ws, s);
+    else if (dt == FP8_DT_BF16)
+        launch_quantise_t<FP8_DT_BF16, FP8_E5M2>(x, rows, cols, ldx, margin, bias_pred, bias, amax_bits, flags, q, ldq, qT, ldqT, ws, s);
+    else if (fmt == FP8_E4M3)
+        launch_quantise_t<FP8_DT_F32, FP8_E4M3>(x, rows, cols, ldx, margin, bias_pred, bias, amax_bits, flags, q, ldq, qT, ldqT, ws, s);
+    else
+        launch_quantise_t<FP8_DT_F32, FP8_E5M2>(x, rows, cols, ldx, margin, bias_pred, bias, amax_bits, flags, q, ldq, qT, ldqT, ws, s);
     return hip_status();
 }
 

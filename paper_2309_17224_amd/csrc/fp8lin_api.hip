@@ -75,6 +75,33 @@ int32_t fp8_scale_bias(const void* x, int32_t dt, int64_t n, int32_t fmt, int32_
                              as_stream(stream));
 }
 
+size_t fp8_quantise_ws_bytes(int64_t rows, int64_t cols) {
+    if (rows <= 0 || cols <= 0 || rows > kMaxDim || cols > kMaxDim) return 0;
+    return (size_t)quantise_ws_words(rows, cols) * sizeof(uint32_t);
+}
+
+int32_t fp8_quantise(const void* x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx,
+                     int32_t fmt, int32_t margin, const int32_t* bias_pred, int32_t* bias,
+                     uint32_t* amax_bits, uint32_t* flags, uint8_t* q, int64_t ldq, uint8_t* qT,
+                     int64_t ldqT, void* ws, size_t ws_bytes, void* stream) {
+    if (!dt_ok(dt) || !fmt_ok(fmt) || rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim)
+        return FP8_EINVAL;
+    if (margin > FP8_MAX_MARGIN || margin < -FP8_MAX_MARGIN) return FP8_EINVAL;
+    if (!bias || !aligned(bias, 4)) return FP8_EINVAL;
+    if ((amax_bits && !aligned(amax_bits, 4)) || (flags && !aligned(flags, 4))) return FP8_EINVAL;
+    if (bias_pred && !aligned(bias_pred, 4)) return FP8_EINVAL;
+    if (rows == 0 || cols == 0)  // amax 0: bias 0 and the zero flag, nothing to cast
+        return launch_scale_bias(x, dt, 0, fmt, margin, bias, amax_bits, flags, nullptr,
+                                 as_stream(stream));
+    if (!x || (!q && !qT) || !ws) return FP8_EINVAL;
+    if (!aligned(x, esize(dt)) || !aligned(ws, 4)) return FP8_EINVAL;
+    if (ldx < cols || (q && ldq < cols) || (qT && ldqT < rows)) return FP8_EINVAL;
+    if (ws_bytes < fp8_quantise_ws_bytes(rows, cols)) return FP8_EINVAL;
+    if (quantise_ws_words(rows, cols) - 1 > INT32_MAX) return FP8_ENOTSUP;
+    return launch_quantise(x, dt, rows, cols, ldx, fmt, margin, bias_pred, bias, amax_bits, flags,
+                           q, ldq, qT, ldqT, (uint32_t*)ws, as_stream(stream));
+}
+
 int32_t fp8_bias_from_amax(const uint32_t* amax_bits, int32_t fmt, int32_t margin, int32_t* bias,
                            uint32_t* flags, void* stream) {
     if (!fmt_ok(fmt) || margin < -FP8_MAX_MARGIN || margin > FP8_MAX_MARGIN) return FP8_EINVAL;

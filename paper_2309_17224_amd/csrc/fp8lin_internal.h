@@ -25,6 +25,14 @@ int32_t launch_cast(const void* x, int dt, int64_t rows, int64_t cols, int64_t l
                     const int32_t* bias, uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT,
                     hipStream_t s);
 
+// amax + bias + cast of a rows x cols tensor (two kernels); ws holds
+// quantise_ws_words(rows, cols) uint32 words.
+int64_t quantise_ws_words(int64_t rows, int64_t cols);
+int32_t launch_quantise(const void* x, int dt, int64_t rows, int64_t cols, int64_t ldx, int fmt,
+                        int32_t margin, const int32_t* bias_pred, int32_t* bias, uint32_t* amax_bits,
+                        uint32_t* flags, uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT,
+                        uint32_t* ws, hipStream_t s);
+
 // C[m, n] = 2^-(*ba + *bb) * sum_k A[m, k] * B[n, k]; A [M, K] (format fa),
 // B [N, K] (format fb), both dense; C [M, N] dense of type out_dt.
 int32_t launch_gemm_nt(const uint8_t* A, int fa, const int32_t* ba, const uint8_t* B, int fb,

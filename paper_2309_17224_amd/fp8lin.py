@@ -25,7 +25,8 @@ OK, EINVAL, ENOTSUP, EHIP = 0, 1, 2, 3
 # Every symbol declared in include/fp8lin.h.
 EXPORTS = (
     "fp8_status_string", "fp8_abi_version", "fp8_scale_bias_ws_bytes", "fp8_scale_bias",
-    "fp8_bias_from_amax", "fp8_cast_e4", "fp8_cast_e5", "fp8_linear_fwd", "fp8_linear_bwd_dx",
+    "fp8_bias_from_amax", "fp8_cast_e4", "fp8_cast_e5", "fp8_quantise_ws_bytes", "fp8_quantise",
+    "fp8_linear_fwd", "fp8_linear_bwd_dx",
     "fp8_linear_bwd_dw", "ptq_quantise_weights",
 )
 
@@ -61,6 +62,11 @@ def lib() -> ctypes.CDLL:
             f = getattr(L, name)
             f.restype = i32
             f.argtypes = [vp, i32, i64, i64, i64, vp, vp, i64, vp, i64, vp]
+        L.fp8_quantise_ws_bytes.restype = sz
+        L.fp8_quantise_ws_bytes.argtypes = [i64, i64]
+        L.fp8_quantise.restype = i32
+        L.fp8_quantise.argtypes = [vp, i32, i64, i64, i64, i32, i32, vp, vp, vp, vp, vp, i64, vp,
+                                   i64, vp, sz, vp]
         for name in ("fp8_linear_fwd", "fp8_linear_bwd_dx"):
             f = getattr(L, name)
             f.restype = i32
@@ -166,6 +172,40 @@ def fp8_cast_e4(x, bias, q=None, qT=None, want_q=True, want_qT=False, stream=Non
 def fp8_cast_e5(x, bias, q=None, qT=None, want_q=True, want_qT=False, stream=None):
     """Scale by 2^bias and cast to E5M2; returns (q, qT)."""
     return _cast("fp8_cast_e5", x, bias, q, qT, want_q, want_qT, stream)
+
+
+def fp8_quantise_ws_bytes(rows: int, cols: int) -> int:
+    return int(lib().fp8_quantise_ws_bytes(rows, cols))
+
+
+def quantise_workspace(rows: int, cols: int, device) -> torch.Tensor:
+    return torch.empty(max(fp8_quantise_ws_bytes(rows, cols), 4), dtype=torch.uint8, device=device)
+
+
+def fp8_quantise(x: torch.Tensor, fmt: int, margin: int = 0, bias_pred=None, bias=None,
+                 amax_bits=None, flags=None, q=None, qT=None, want_q=True, want_qT=False, ws=None,
+                 stream=None):
+    """amax + Eq. 3 bias + cast of a whole 2-D tensor (codes and/or transposed
+    codes).  bias_pred: optional one-element device tensor with a predicted
+    bias (may be `bias` itself).  Returns (q, qT, bias, amax_bits, flags)."""
+    x2 = x if x.dim() == 2 else x.reshape(1, -1)
+    rows, cols = x2.shape
+    dev = x.device
+    bias = _i32(dev) if bias is None else bias
+    amax_bits = _i32(dev) if amax_bits is None else amax_bits
+    flags = _i32(dev) if flags is None else flags
+    if want_q and q is None:
+        q = torch.empty((rows, cols), dtype=torch.uint8, device=dev)
+    if want_qT and qT is None:
+        qT = torch.empty((cols, rows), dtype=torch.uint8, device=dev)
+    ws = quantise_workspace(rows, cols, dev) if ws is None else ws
+    st = lib().fp8_quantise(_p(x2), _dt(x2), rows, cols, _ld(x2), fmt, margin, _p(bias_pred),
+                            _p(bias), _p(amax_bits), _p(flags), _p(q),
+                            _ld(q) if q is not None else 0, _p(qT),
+                            _ld(qT) if qT is not None else 0, _p(ws),
+                            ws.numel() * ws.element_size(), _stream(stream))
+    _check("fp8_quantise", st)
+    return q, qT, bias, amax_bits, flags
 
 
 def _out(shape, out_dt, dev, out):

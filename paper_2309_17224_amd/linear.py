@@ -167,16 +167,30 @@ class WorkloadStep:
     are scaled and cast per call, weights once beforehand (PTQ).
     ``calls`` lists (label, kind, flops_or_bytes, fn); running them in order
     is one step.
+
+    quant: how each tensor gets its bias and codes.
+      "predicted": fp8_quantise with the tensor's previous bias as the
+                   prediction (one read of the tensor when it is unchanged);
+      "twopass":   fp8_quantise without a prediction (amax pass, then cast);
+      "separate":  fp8_scale_bias followed by fp8_cast_e4/e5.
+    All three give identical bits.
     """
 
-    def __init__(self, workload, tensors: dict, device, margin: int = 0):
+    QUANT_MODES = ("predicted", "twopass", "separate")
+
+    def __init__(self, workload, tensors: dict, device, margin: int = 0, quant: str = "predicted"):
+        if quant not in self.QUANT_MODES:
+            raise ValueError(f"quant must be one of {self.QUANT_MODES}")
         self.w = workload
         self.t = tensors
         self.dev = torch.device(device)
         self.margin = margin
+        self.quant = quant
         lin = workload.linears
         nmax = max(x.numel() for x in tensors.values())
         self.ws = F.workspace(nmax, device)
+        qws = max(F.fp8_quantise_ws_bytes(*x.shape) for x in tensors.values())
+        self.qws = torch.empty(max(qws, 4), dtype=torch.uint8, device=device)
         self.q = {}
         train = workload.train
         for l in lin:
@@ -203,6 +217,15 @@ class WorkloadStep:
         qt = self.q[name]
         cast = F.fp8_cast_e4 if fmt == F.E4M3 else F.fp8_cast_e5
         n = x.numel()
+        code_bytes = n + (n if qt.qT is not None and qt.q is not None else 0)
+        if self.quant != "separate":
+            pred = qt.bias if self.quant == "predicted" else None
+            # one read of the tensor and its codes when the prediction holds
+            return [(f"quantise {name}", "quantise", 2 * n + code_bytes,
+                     lambda: F.fp8_quantise(x, fmt, margin, bias_pred=pred, bias=qt.bias,
+                                            amax_bits=qt.amax, flags=qt.flags, q=qt.q, qT=qt.qT,
+                                            want_q=qt.q is not None, want_qT=qt.qT is not None,
+                                            ws=self.qws))]
         return [
             (f"amax+bias {name}", "amax", 2 * n,
              lambda: F.fp8_scale_bias(x, fmt, margin, bias=qt.bias, amax_bits=qt.amax,

@@ -82,3 +82,24 @@ def test_graph_replay_reads_current_inputs(gpu):
     assert torch.equal(_bits(out[f"{lin.name}.y"]), _bits(ref[f"{lin.name}.y"] * 2))
     assert torch.equal(_bits(out[f"{lin.name}.dw"]), _bits(ref[f"{lin.name}.dw"] * 2))
     assert torch.equal(_bits(out[f"{lin.name}.dx"]), _bits(ref[f"{lin.name}.dx"]))
+
+
+def test_step_quant_modes_identical(gpu):
+    """Predicted-bias quantise, two-pass quantise and the separate amax + cast
+    calls give the same bits for every output of the step, eager and replayed
+    (the predicted mode is right after the first step and wrong in the first)."""
+    w = wl.WORKLOADS["gpt111m-linear"]
+    tens = {t.name: wl.make_tensor(w, t.name).to(gpu) for t in w.tensors}
+    outs = {}
+    for mode in L.WorkloadStep.QUANT_MODES:
+        step = L.WorkloadStep(w, tens, gpu, quant=mode)
+        step.run()
+        step.capture()
+        step.replay()
+        step.replay()
+        torch.cuda.synchronize()
+        outs[mode] = {k: v.clone() for k, v in _outputs(step).items()}
+    ref = outs["separate"]
+    for mode in ("predicted", "twopass"):
+        for k, v in outs[mode].items():
+            assert torch.equal(_bits(v), _bits(ref[k])), f"{mode}: {k} differs"
