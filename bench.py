@@ -46,10 +46,12 @@ def parse():
                    help="seconds of oracle GEMM work in the CPU baseline sample")
     p.add_argument("--flush-mb", type=int, default=0,
                    help="write this many MB before every step (evicts the 256 MB MALL)")
-    p.add_argument("--quant", choices=("predicted", "twopass", "separate"), default="predicted",
+    p.add_argument("--quant", choices=("predicted", "twopass", "separate", "cscale"), default="predicted",
                    help="bias + cast of X, W, dY: one fp8_quantise call predicting each bias from "
                         "the previous step (identical bits; one read of an unchanged tensor), "
-                        "fp8_quantise without prediction, or fp8_scale_bias + fp8_cast")
+                        "fp8_quantise without prediction, fp8_scale_bias + fp8_cast, or FP8-CSCALE "
+                        "(constant bias --cscale-bias, no amax: not the headline metric)")
+    p.add_argument("--cscale-bias", type=int, default=0)
     p.add_argument("--launch", choices=("graph", "eager"), default="graph",
                    help="timed steps: replays of one HIP graph holding the whole step, or "
                         "one host call per library call")
@@ -270,7 +272,8 @@ def main():
     cpu = make_inputs(w)
     tens = {k: v.to(dev) for k, v in cpu.items()}
     torch.cuda.synchronize()
-    step = L.WorkloadStep(w, tens, dev, margin=args.margin, quant=args.quant)
+    step = L.WorkloadStep(w, tens, dev, margin=args.margin, quant=args.quant,
+                          cscale_bias=args.cscale_bias)
     if not w.train:
         step.prepare_inference()
     flush = None

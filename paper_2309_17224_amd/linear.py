@@ -173,12 +173,16 @@ class WorkloadStep:
                    prediction (one read of the tensor when it is unchanged);
       "twopass":   fp8_quantise without a prediction (amax pass, then cast);
       "separate":  fp8_scale_bias followed by fp8_cast_e4/e5.
-    All three give identical bits.
+    All three give identical bits (FP8-AMAX, Sec. 2.3).
+      "cscale":    FP8-CSCALE (Sec. 3): one constant bias `cscale_bias` for every
+                   weight, activation and gradient; no amax, only the casts and
+                   the matmuls (no epilogue amax either).
     """
 
-    QUANT_MODES = ("predicted", "twopass", "separate")
+    QUANT_MODES = ("predicted", "twopass", "separate", "cscale")
 
-    def __init__(self, workload, tensors: dict, device, margin: int = 0, quant: str = "predicted"):
+    def __init__(self, workload, tensors: dict, device, margin: int = 0, quant: str = "predicted",
+                 cscale_bias: int = 0):
         if quant not in self.QUANT_MODES:
             raise ValueError(f"quant must be one of {self.QUANT_MODES}")
         self.w = workload
@@ -186,6 +190,7 @@ class WorkloadStep:
         self.dev = torch.device(device)
         self.margin = margin
         self.quant = quant
+        self.cscale_bias = int(cscale_bias)
         lin = workload.linears
         nmax = max(x.numel() for x in tensors.values())
         self.ws = F.workspace(nmax, device)
@@ -218,6 +223,11 @@ class WorkloadStep:
         cast = F.fp8_cast_e4 if fmt == F.E4M3 else F.fp8_cast_e5
         n = x.numel()
         code_bytes = n + (n if qt.qT is not None and qt.q is not None else 0)
+        if self.quant == "cscale":
+            qt.bias.fill_(self.cscale_bias)
+            return [(f"cast {name}", "cast", 2 * n + code_bytes,
+                     lambda: cast(x, qt.bias, q=qt.q, qT=qt.qT, want_q=qt.q is not None,
+                                  want_qT=qt.qT is not None))]
         if self.quant != "separate":
             pred = qt.bias if self.quant == "predicted" else None
             # one read of the tensor and its codes when the prediction holds
@@ -256,11 +266,12 @@ class WorkloadStep:
             kind, work = "gemm_fwd", flop
             if l.M <= 32:
                 kind, work = "gemm_decode", l.N * l.K + l.M * l.K + 2 * l.M * l.N
+            amax_y = self.w.train and self.quant != "cscale"
             calls.append((f"fwd {l.name}", kind, work,
-                          lambda xq=xq, wq=wq, o=o: F.fp8_linear_fwd(
+                          lambda xq=xq, wq=wq, o=o, amax_y=amax_y: F.fp8_linear_fwd(
                               xq.q, xq.bias, wq.qT, wq.bias, y=o["y"],
-                              y_amax_bits=o["y_scal"][1:2] if self.w.train else None)))
-            if self.w.train:
+                              y_amax_bits=o["y_scal"][1:2] if amax_y else None)))
+            if amax_y:
                 calls.append((f"bias y {l.name}", "bias", 0,
                               lambda o=o: F.fp8_bias_from_amax(o["y_scal"][1:2], F.E4M3, 0,
                                                                bias=o["y_scal"][0:1],
@@ -273,14 +284,16 @@ class WorkloadStep:
             for l in lin:
                 xq, wq, gq, o = self.q[l.x], self.q[l.w], self.q[l.dy], self.out[l.name]
                 flop = 2 * l.M * l.N * l.K
+                amax_dx = self.quant != "cscale"
                 calls.append((f"dx {l.name}", "gemm_dx", flop,
-                              lambda wq=wq, gq=gq, o=o: F.fp8_linear_bwd_dx(
+                              lambda wq=wq, gq=gq, o=o, amax_dx=amax_dx: F.fp8_linear_bwd_dx(
                                   gq.q, gq.bias, wq.q, wq.bias, dx=o["dx"],
-                                  dx_amax_bits=o["dx_scal"][1:2])))
-                calls.append((f"bias dx {l.name}", "bias", 0,
-                              lambda o=o: F.fp8_bias_from_amax(o["dx_scal"][1:2], F.E5M2,
-                                                               self.margin, bias=o["dx_scal"][0:1],
-                                                               flags=o["dx_scal"][2:3])))
+                                  dx_amax_bits=o["dx_scal"][1:2] if amax_dx else None)))
+                if amax_dx:
+                    calls.append((f"bias dx {l.name}", "bias", 0,
+                                  lambda o=o: F.fp8_bias_from_amax(o["dx_scal"][1:2], F.E5M2,
+                                                                   self.margin, bias=o["dx_scal"][0:1],
+                                                                   flags=o["dx_scal"][2:3])))
                 calls.append((f"dw {l.name}", "gemm_dw", flop,
                               lambda xq=xq, gq=gq, o=o: F.fp8_linear_bwd_dw(
                                   xq.qT, xq.bias, gq.qT, gq.bias, dw=o["dw"])))

@@ -81,6 +81,31 @@ def test_cast_rejects(L):
         assert f(NULL, 0, 0, 8, 8, NULL, NULL, 8, NULL, 4, NULL) == F.OK       # empty: no-op
 
 
+def test_quantise_workspace_size(L):
+    assert L.fp8_quantise_ws_bytes(0, 5) == 0
+    assert L.fp8_quantise_ws_bytes(128, 128) == 4 * (1 + 1)
+    assert L.fp8_quantise_ws_bytes(129, 300) == 4 * (1 + 2 * 3)
+
+
+def test_quantise_rejects(L):
+    f = L.fp8_quantise
+    WS = 4 * 64
+    #        x     dt rows cols ldx fmt marg pred  bias  amax  flags q     ldq qT    ldqT ws    wsb  stream
+    assert f(FAKE, 0, 4, 8, 8, 0, 0, NULL, FAKE, NULL, NULL, NULL, 8, NULL, 4, FAKE, WS, NULL) == F.EINVAL  # no output
+    assert f(FAKE, 0, 4, 8, 7, 0, 0, NULL, FAKE, NULL, NULL, FAKE, 8, NULL, 4, FAKE, WS, NULL) == F.EINVAL  # ldx
+    assert f(FAKE, 0, 4, 8, 8, 0, 0, NULL, FAKE, NULL, NULL, FAKE, 7, NULL, 4, FAKE, WS, NULL) == F.EINVAL  # ldq
+    assert f(FAKE, 0, 4, 8, 8, 0, 0, NULL, FAKE, NULL, NULL, NULL, 0, FAKE, 3, FAKE, WS, NULL) == F.EINVAL  # ldqT
+    assert f(NULL, 0, 4, 8, 8, 0, 0, NULL, FAKE, NULL, NULL, FAKE, 8, NULL, 4, FAKE, WS, NULL) == F.EINVAL  # x
+    assert f(FAKE, 0, 4, 8, 8, 0, 0, NULL, NULL, NULL, NULL, FAKE, 8, NULL, 4, FAKE, WS, NULL) == F.EINVAL  # bias
+    assert f(FAKE, 0, 4, 8, 8, 0, 0, ODD, FAKE, NULL, NULL, FAKE, 8, NULL, 4, FAKE, WS, NULL) == F.EINVAL   # pred align
+    assert f(FAKE, 0, 4, 8, 8, 0, 0, NULL, FAKE, NULL, NULL, FAKE, 8, NULL, 4, NULL, WS, NULL) == F.EINVAL  # ws
+    assert f(FAKE, 0, 4, 8, 8, 0, 0, NULL, FAKE, NULL, NULL, FAKE, 8, NULL, 4, FAKE, 4, NULL) == F.EINVAL   # ws small
+    assert f(FAKE, 3, 4, 8, 8, 0, 0, NULL, FAKE, NULL, NULL, FAKE, 8, NULL, 4, FAKE, WS, NULL) == F.EINVAL  # dtype
+    assert f(FAKE, 0, 4, 8, 8, 2, 0, NULL, FAKE, NULL, NULL, FAKE, 8, NULL, 4, FAKE, WS, NULL) == F.EINVAL  # format
+    assert f(FAKE, 0, 4, 8, 8, 0, 1 << 20, NULL, FAKE, NULL, NULL, FAKE, 8, NULL, 4, FAKE, WS, NULL) == F.EINVAL  # margin
+    assert f(FAKE, 0, -1, 8, 8, 0, 0, NULL, FAKE, NULL, NULL, FAKE, 8, NULL, 4, FAKE, WS, NULL) == F.EINVAL  # rows < 0
+
+
 def test_gemm_rejects(L):
     for f in (L.fp8_linear_fwd, L.fp8_linear_bwd_dx):
         assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 3, 4, 4, 4, NULL, NULL) == F.EINVAL    # out dtype

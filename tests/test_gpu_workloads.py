@@ -151,3 +151,37 @@ def test_ptq_entry_matches_oracle(orc, gpu):
     assert (i32(bw), u32(fl)) == (obw, ofl)
     assert np.array_equal(w8.cpu().numpy(), ow8)
     assert np.array_equal(w8t.cpu().numpy(), ow8t)
+
+
+@pytest.mark.parametrize("cbias", [0, 3, -2])
+def test_cscale_step_parity(orc, gpu, cbias):
+    """FP8-CSCALE (Sec. 3): every tensor cast with one constant bias, no amax.
+    Codes bit-exact against the oracle's cast with that bias (App. A clipping
+    included: a constant bias can push values past the largest code); the
+    matmuls rel_F <= 1e-3 against the oracle on the same codes."""
+    w = wl.WORKLOADS["gpt111m-linear"]
+    lin = w.linears[0]
+    tens = {t.name: tensor(w.name, t.name).to(gpu) for t in w.tensors}
+    step = L.WorkloadStep(w, tens, gpu, quant="cscale", cscale_bias=cbias)
+    step.run()
+    torch.cuda.synchronize()
+    assert not any(k == "amax" or k == "quantise" or k == "bias" for _, k, _, _ in step.calls)
+    xq, wq, gq = step.q[lin.x], step.q[lin.w], step.q[lin.dy]
+    for qt in (xq, wq, gq):
+        assert i32(qt.bias) == cbias
+    X, W, dY = (np_bits(tensor(w.name, n)) for n in (lin.x, lin.w, lin.dy))
+    x8, x8t = orc.cast(X, orc.E4M3, cbias, transpose=True)
+    w8, w8t = orc.cast(W, orc.E4M3, cbias, transpose=True)
+    g8, g8t = orc.cast(dY, orc.E5M2, cbias, transpose=True)
+    assert np.array_equal(xq.q.cpu().numpy(), x8) and np.array_equal(xq.qT.cpu().numpy(), x8t)
+    assert np.array_equal(wq.q.cpu().numpy(), w8) and np.array_equal(wq.qT.cpu().numpy(), w8t)
+    assert np.array_equal(gq.q.cpu().numpy(), g8) and np.array_equal(gq.qT.cpu().numpy(), g8t)
+    o = step.out[lin.name]
+    rows = sample_rows(lin.M, 128, 7)
+    yref = orc.gemm_nt(x8, 0, cbias, w8t, 0, cbias, out_dt=orc.BF16, rows=rows)
+    assert rel_f(np_bits(o["y"])[rows], yref) <= REL_F_TOL
+    dxref = orc.gemm_nt(g8, 1, cbias, w8, 0, cbias, out_dt=orc.BF16, rows=rows)
+    assert rel_f(np_bits(o["dx"])[rows], dxref) <= REL_F_TOL
+    rdw = sample_rows(lin.K, 128, 8)
+    dwref = orc.gemm_nt(x8t, 0, cbias, g8t, 1, cbias, out_dt=orc.F32, rows=rdw)
+    assert rel_f(np_bits(o["dw"])[rdw], dwref) <= REL_F_TOL
