@@ -64,9 +64,16 @@ extern "C" {
 #define FP8_ENOTSUP 2  /* valid but unsupported combination */
 #define FP8_EHIP 3     /* the HIP runtime reported a launch error */
 
-/* FP8 formats (OCP; Table 7 rows "(b)"). */
+/* FP8 formats.  OCP (Table 7 rows "(b)"), the formats of the matrix cores: */
 #define FP8_E4M3 0
 #define FP8_E5M2 1
+/* The paper's own formats (Table 7 rows "(a)"): E4 bias 8, largest finite 240;
+ * E5 bias 16, largest finite 57344; code 0x80 is the only NaN, no infinity,
+ * no -0.  Accepted by the bias and cast calls (fp8_scale_bias,
+ * fp8_bias_from_amax, fp8_cast, fp8_quantise), not by the matmuls.  Every code
+ * finite in both families decodes in (a) to half its OCP value. */
+#define FP8_E4_A 2
+#define FP8_E5_A 3
 
 /* Higher-precision element types of inputs and outputs. */
 #define FP8_DT_BF16 0
@@ -139,6 +146,15 @@ int32_t fp8_cast_e4(const void *x, int32_t dt, int64_t rows, int64_t cols, int64
 int32_t fp8_cast_e5(const void *x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx,
                     const int32_t *bias, uint8_t *q, int64_t ldq, uint8_t *qT, int64_t ldqT,
                     void *stream);
+
+/*
+ * fp8_cast -- fp8_cast_e4 / fp8_cast_e5 with the format as an argument: any of
+ * FP8_E4M3, FP8_E5M2, FP8_E4_A, FP8_E5_A.  In the (a) formats, NaN becomes 0x80
+ * and values that round to zero become 0x00 whatever their sign.
+ */
+int32_t fp8_cast(const void *x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx,
+                 int32_t fmt, const int32_t *bias, uint8_t *q, int64_t ldq, uint8_t *qT,
+                 int64_t ldqT, void *stream);
 
 /*
  * fp8_quantise -- amax, Eq. 3 bias and scale+cast of one whole tensor in one

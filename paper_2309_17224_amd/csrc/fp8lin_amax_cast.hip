@@ -20,27 +20,56 @@
 // detected with a packed integer test, are re-encoded as 0x7F with their sign.
 // The transposed copy goes through a 128 x 128 byte LDS tile so that both
 // outputs leave as coalesced stores (whole 128-byte lines for the transpose).
+#include <type_traits>
+
 #include "fp8lin_internal.h"
 
 namespace fp8lin {
 namespace {
 
 // ---------------------------------------------------------------- formats
-// OCP FP8 (Table 7 rows "(b)"): largest finite value 1.75 * 2^kMaxExp.
+// Largest finite value f_M * 2^kMaxExp, with f_M = 1.75 (kMantMax 0x600000 as
+// fp32 mantissa bits) or 1.875 (0x700000).
+// OCP FP8 (Table 7 rows "(b)"): converted by the hardware.
+// The paper's formats (rows "(a)": E4 bias 8, max 240; E5 bias 16, max 57344;
+// one NaN code 0x80, no infinity, no -0): every code finite in both families
+// decodes in (a) to half its OCP value, so the (a) code of x at bias b is the
+// OCP code of x * 2^(b + 1) (kShift), except where (a) has values above the OCP
+// maximum, for -0 (0x00 in (a)) and for NaN (0x80 in (a)).
 template <int FMT> struct Fmt;
 template <> struct Fmt<FP8_E4M3> {
     static constexpr int kMaxExp = 8;  // max finite = 1.75 * 2^8 = 448
-    static constexpr float kMax = 448.0f;
+    static constexpr uint32_t kMantMax = 0x600000u;
+    static constexpr float kMax = 448.0f;  // hardware clip (OCP maximum)
+    static constexpr int kShift = 0, kHw = FP8_E4M3;
+    static constexpr bool kPaper = false;
 };
 template <> struct Fmt<FP8_E5M2> {
     static constexpr int kMaxExp = 15;  // max finite = 1.75 * 2^15 = 57344
+    static constexpr uint32_t kMantMax = 0x600000u;
     static constexpr float kMax = 57344.0f;
+    static constexpr int kShift = 0, kHw = FP8_E5M2;
+    static constexpr bool kPaper = false;
+};
+template <> struct Fmt<FP8_E4_A> {
+    static constexpr int kMaxExp = 7;  // max finite = 1.875 * 2^7 = 240
+    static constexpr uint32_t kMantMax = 0x700000u;
+    static constexpr float kMax = 448.0f;
+    static constexpr int kShift = 1, kHw = FP8_E4M3;
+    static constexpr bool kPaper = true;
+};
+template <> struct Fmt<FP8_E5_A> {
+    static constexpr int kMaxExp = 15;  // max finite = 1.75 * 2^15 = 57344
+    static constexpr uint32_t kMantMax = 0x600000u;
+    static constexpr float kMax = 57344.0f;
+    static constexpr int kShift = 1, kHw = FP8_E5M2;
+    static constexpr bool kPaper = true;
 };
 
 constexpr int kBiasClamp = 512;  // beyond this every input saturates or flushes
 
 // Eq. 3 on the fp32 bit pattern of the amax: with amax = 1.f_a * 2^ea and
-// max_num = 1.75 * 2^eM, floor(log2(max_num / amax)) = eM - ea - [1.f_a > 1.75].
+// max_num = f_M * 2^eM, floor(log2(max_num / amax)) = eM - ea - [1.f_a > f_M].
 template <int FMT>
 __device__ __forceinline__ int32_t bias_of(uint32_t u, int32_t margin, uint32_t* fl) {
     u &= 0x7FFFFFFFu;
@@ -57,7 +86,7 @@ __device__ __forceinline__ int32_t bias_of(uint32_t u, int32_t margin, uint32_t*
     } else {
         ea = e - 127;
     }
-    const int b = Fmt<FMT>::kMaxExp - ea - (mant > 0x600000u ? 1 : 0);
+    const int b = Fmt<FMT>::kMaxExp - ea - (mant > Fmt<FMT>::kMantMax ? 1 : 0);
     return b - margin;
 }
 
@@ -177,40 +206,91 @@ __global__ void bias_from_amax_kernel(const uint32_t* __restrict__ amax_bits, in
 
 // ---------------------------------------------------------------- cast
 // Two scaled, clipped values -> two codes in the low (HI = false) or high
-// half of `old`.
+// half of `old`, by the hardware converter of the format's OCP counterpart.
 template <int FMT, bool HI>
 __device__ __forceinline__ uint32_t cvt2(float a, float b, uint32_t old) {
-    if (FMT == FP8_E4M3) return __builtin_amdgcn_cvt_pk_fp8_f32(a, b, old, HI);
+    if (Fmt<FMT>::kHw == FP8_E4M3) return __builtin_amdgcn_cvt_pk_fp8_f32(a, b, old, HI);
     return __builtin_amdgcn_cvt_pk_bf8_f32(a, b, old, HI);
 }
 
+// x * 2^(b + kShift): exact (a power-of-two scale).
 template <int FMT>
-__device__ __forceinline__ float scale_clip(float f, int b) {
-    return __builtin_amdgcn_fmed3f(ldexpf(f, b), -Fmt<FMT>::kMax, Fmt<FMT>::kMax);
+__device__ __forceinline__ float scaled(float f, int b) { return ldexpf(f, b + Fmt<FMT>::kShift); }
+
+// Clip to the OCP maximum before the hardware conversion (App. A: overflow
+// clips to the maximum, infinities included).
+template <int FMT>
+__device__ __forceinline__ float clip(float y) {
+    return __builtin_amdgcn_fmed3f(y, -Fmt<FMT>::kMax, Fmt<FMT>::kMax);
+}
+
+// (a) formats, |y| (scaled by 2^(b+1)) above the OCP maximum: magnitude code
+// among the (a) codes beyond it, to nearest with ties to the even mantissa,
+// clipping at the (a) maximum.  E4: 0x7E = 448 and 0x7F = 480 in these units.
+// E5: 0x7B = 57344, 0x7C..0x7F = 65536, 81920, 98304, 114688.
+template <int FMT>
+__device__ __forceinline__ uint32_t top_code(float a) {
+    if (FMT == FP8_E4_A) return a > 464.0f ? 0x7Fu : 0x7Eu;
+    return a < 61440.0f ? 0x7Bu : a <= 73728.0f ? 0x7Cu : a < 90112.0f ? 0x7Du : a <= 106496.0f ? 0x7Eu : 0x7Fu;
+}
+
+// (a) formats: fix-ups of four hardware codes for the scaled values y[4]
+// (before the NaN patch): -0 (0x80) becomes 0x00, values beyond the OCP
+// maximum get their (a) code.  OCP formats: unchanged.
+template <int FMT>
+__device__ __forceinline__ uint32_t paper_fix(uint32_t c, const float y[4]) {
+    if (!Fmt<FMT>::kPaper) return c;
+    const uint32_t v = c ^ 0x80808080u;  // bytes that were 0x80 are now 0
+    const uint32_t z = ~(((v & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | v) & 0x80808080u;
+    c &= ~((z >> 7) * 0xFFu);
+    const float m = fmaxf(fmaxf(fabsf(y[0]), fabsf(y[1])), fmaxf(fabsf(y[2]), fabsf(y[3])));
+    if (__builtin_expect(m > Fmt<FMT>::kMax, 0)) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float a = fabsf(y[e]);
+            if (a > Fmt<FMT>::kMax)
+                c = (c & ~(0xFFu << (8 * e))) | ((top_code<FMT>(a) | (y[e] < 0.0f ? 0x80u : 0u)) << (8 * e));
+        }
+    }
+    return c;
+}
+
+// Four scaled values -> four codes, before the NaN patch.
+template <int FMT>
+__device__ __forceinline__ uint32_t cast4(const float y[4]) {
+    const uint32_t c = cvt2<FMT, false>(clip<FMT>(y[0]), clip<FMT>(y[1]), 0u);
+    return paper_fix<FMT>(cvt2<FMT, true>(clip<FMT>(y[2]), clip<FMT>(y[3]), c), y);
 }
 
 // Four bf16 values (two packed words) -> four codes, before the NaN patch.
 template <int FMT>
 __device__ __forceinline__ uint32_t cast4_bf16(uint32_t w0, uint32_t w1, int b) {
-    const float f0 = __uint_as_float(w0 << 16), f1 = __uint_as_float(w0 & 0xFFFF0000u);
-    const float f2 = __uint_as_float(w1 << 16), f3 = __uint_as_float(w1 & 0xFFFF0000u);
-    const uint32_t c = cvt2<FMT, false>(scale_clip<FMT>(f0, b), scale_clip<FMT>(f1, b), 0u);
-    return cvt2<FMT, true>(scale_clip<FMT>(f2, b), scale_clip<FMT>(f3, b), c);
+    const float y[4] = {scaled<FMT>(__uint_as_float(w0 << 16), b), scaled<FMT>(__uint_as_float(w0 & 0xFFFF0000u), b),
+                        scaled<FMT>(__uint_as_float(w1 << 16), b), scaled<FMT>(__uint_as_float(w1 & 0xFFFF0000u), b)};
+    return cast4<FMT>(y);
 }
 
 template <int FMT>
 __device__ __forceinline__ uint32_t cast4_f32(uint4 v, int b) {
-    const uint32_t c = cvt2<FMT, false>(scale_clip<FMT>(__uint_as_float(v.x), b), scale_clip<FMT>(__uint_as_float(v.y), b), 0u);
-    return cvt2<FMT, true>(scale_clip<FMT>(__uint_as_float(v.z), b), scale_clip<FMT>(__uint_as_float(v.w), b), c);
+    const float y[4] = {scaled<FMT>(__uint_as_float(v.x), b), scaled<FMT>(__uint_as_float(v.y), b),
+                        scaled<FMT>(__uint_as_float(v.z), b), scaled<FMT>(__uint_as_float(v.w), b)};
+    return cast4<FMT>(y);
 }
 
-// Re-encode NaN inputs as 0x7F | sign.  hs[e] is input e as a bf16 pattern
-// or as the top half of an fp32 pattern with the low half folded into bit 0
-// (only the NaN test reads it).
+// NaN code: 0x7F with the input's sign (OCP), 0x80 (the paper's formats).
+template <int FMT>
+__device__ __forceinline__ uint32_t nan_code(uint32_t key) {
+    return Fmt<FMT>::kPaper ? 0x80u : (0x7Fu | ((key >> 8) & 0x80u));
+}
+
+// Re-encode NaN inputs.  hs[e] is input e as a bf16 pattern or as the top
+// half of an fp32 pattern with the low half folded into bit 0 (only the NaN
+// test reads it).
+template <int FMT>
 __device__ __forceinline__ uint32_t nan_patch(uint32_t c, const uint32_t hs[4]) {
 #pragma unroll
     for (int e = 0; e < 4; ++e)
-        if ((hs[e] & 0x7FFFu) > 0x7F80u) c = (c & ~(0xFFu << (8 * e))) | ((0x7Fu | ((hs[e] >> 8) & 0x80u)) << (8 * e));
+        if ((hs[e] & 0x7FFFu) > 0x7F80u) c = (c & ~(0xFFu << (8 * e))) | (nan_code<FMT>(hs[e]) << (8 * e));
     return c;
 }
 
@@ -235,8 +315,9 @@ __device__ __forceinline__ uint32_t cast1(const void* x, int64_t idx, int b) {
         key = f32_key(u);
         f = __uint_as_float(u);
     }
-    uint32_t c = cvt2<FMT, false>(scale_clip<FMT>(f, b), 0.0f, 0u) & 0xFFu;
-    if ((key & 0x7FFFu) > 0x7F80u) c = 0x7Fu | ((key >> 8) & 0x80u);
+    const float y[4] = {scaled<FMT>(f, b), 0.0f, 0.0f, 0.0f};
+    uint32_t c = cast4<FMT>(y) & 0xFFu;
+    if ((key & 0x7FFFu) > 0x7F80u) c = nan_code<FMT>(key);
     return c;
 }
 
@@ -288,8 +369,8 @@ __device__ __forceinline__ uint32_t cast_tile(const void* __restrict__ x, int64_
                 if (__builtin_expect(any_nan_bf16(v[i].x, v[i].y) || any_nan_bf16(v[i].z, v[i].w), 0)) {
                     const uint32_t h0[4] = {v[i].x & 0xFFFFu, v[i].x >> 16, v[i].y & 0xFFFFu, v[i].y >> 16};
                     const uint32_t h1[4] = {v[i].z & 0xFFFFu, v[i].z >> 16, v[i].w & 0xFFFFu, v[i].w >> 16};
-                    lo[i] = nan_patch(lo[i], h0);
-                    hi[i] = nan_patch(hi[i], h1);
+                    lo[i] = nan_patch<FMT>(lo[i], h0);
+                    hi[i] = nan_patch<FMT>(hi[i], h1);
                 }
             }
         } else {
@@ -304,8 +385,8 @@ __device__ __forceinline__ uint32_t cast_tile(const void* __restrict__ x, int64_
                 if (__builtin_expect(m == 0x7F800000u, 0)) {  // some exponent field may be all ones
                     const uint32_t h0[4] = {f32_key(a.x), f32_key(a.y), f32_key(a.z), f32_key(a.w)};
                     const uint32_t h1[4] = {f32_key(bb.x), f32_key(bb.y), f32_key(bb.z), f32_key(bb.w)};
-                    lo[i] = nan_patch(lo[i], h0);
-                    hi[i] = nan_patch(hi[i], h1);
+                    lo[i] = nan_patch<FMT>(lo[i], h0);
+                    hi[i] = nan_patch<FMT>(hi[i], h1);
                 }
             }
         }
@@ -494,6 +575,27 @@ void launch_quantise_t(const void* x, int64_t rows, int64_t cols, int64_t ldx, i
                        qT, ldqT, tiles_c, vec_in, vec_q, vec_qT);
 }
 
+// Host dispatch of (element type, format) to kernel template arguments.
+template <int V> using IC = std::integral_constant<int, V>;
+
+template <typename Fn>
+void with_fmt(int fmt, Fn&& fn) {
+    switch (fmt) {
+        case FP8_E4M3: fn(IC<FP8_E4M3>{}); break;
+        case FP8_E5M2: fn(IC<FP8_E5M2>{}); break;
+        case FP8_E4_A: fn(IC<FP8_E4_A>{}); break;
+        default: fn(IC<FP8_E5_A>{}); break;
+    }
+}
+
+template <typename Fn>
+void with_dt_fmt(int dt, int fmt, Fn&& fn) {
+    if (dt == FP8_DT_BF16)
+        with_fmt(fmt, [&](auto F) { fn(IC<FP8_DT_BF16>{}, F); });
+    else
+        with_fmt(fmt, [&](auto F) { fn(IC<FP8_DT_F32>{}, F); });
+}
+
 }  // namespace
 
 int amax_blocks(int64_t n) {
@@ -513,37 +615,27 @@ int32_t launch_scale_bias(const void* x, int dt, int64_t n, int fmt, int32_t mar
         hipLaunchKernelGGL(amax_partial_kernel<FP8_DT_BF16>, dim3(nb), dim3(kAmaxThreads), 0, s, x, n, vec, partials);
     else if (nb > 0)
         hipLaunchKernelGGL(amax_partial_kernel<FP8_DT_F32>, dim3(nb), dim3(kAmaxThreads), 0, s, x, n, vec, partials);
-    if (dt == FP8_DT_BF16 && fmt == FP8_E4M3)
-        hipLaunchKernelGGL((amax_finalize_kernel<FP8_DT_BF16, FP8_E4M3>), dim3(1), dim3(kAmaxThreads), 0, s, partials, nb, margin, bias, amax_bits, flags);
-    else if (dt == FP8_DT_BF16)
-        hipLaunchKernelGGL((amax_finalize_kernel<FP8_DT_BF16, FP8_E5M2>), dim3(1), dim3(kAmaxThreads), 0, s, partials, nb, margin, bias, amax_bits, flags);
-    else if (fmt == FP8_E4M3)
-        hipLaunchKernelGGL((amax_finalize_kernel<FP8_DT_F32, FP8_E4M3>), dim3(1), dim3(kAmaxThreads), 0, s, partials, nb, margin, bias, amax_bits, flags);
-    else
-        hipLaunchKernelGGL((amax_finalize_kernel<FP8_DT_F32, FP8_E5M2>), dim3(1), dim3(kAmaxThreads), 0, s, partials, nb, margin, bias, amax_bits, flags);
+    with_dt_fmt(dt, fmt, [&](auto D, auto F) {
+        hipLaunchKernelGGL((amax_finalize_kernel<decltype(D)::value, decltype(F)::value>), dim3(1), dim3(kAmaxThreads), 0,
+                           s, partials, nb, margin, bias, amax_bits, flags);
+    });
     return hip_status();
 }
 
 int32_t launch_bias_from_amax(const uint32_t* amax_bits, int fmt, int32_t margin, int32_t* bias,
                               uint32_t* flags, hipStream_t s) {
-    if (fmt == FP8_E4M3)
-        hipLaunchKernelGGL(bias_from_amax_kernel<FP8_E4M3>, dim3(1), dim3(64), 0, s, amax_bits, margin, bias, flags);
-    else
-        hipLaunchKernelGGL(bias_from_amax_kernel<FP8_E5M2>, dim3(1), dim3(64), 0, s, amax_bits, margin, bias, flags);
+    with_fmt(fmt, [&](auto F) {
+        hipLaunchKernelGGL(bias_from_amax_kernel<decltype(F)::value>, dim3(1), dim3(64), 0, s, amax_bits, margin, bias, flags);
+    });
     return hip_status();
 }
 
 int32_t launch_cast(const void* x, int dt, int64_t rows, int64_t cols, int64_t ldx, int fmt,
                     const int32_t* bias, uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT,
                     hipStream_t s) {
-    if (dt == FP8_DT_BF16 && fmt == FP8_E4M3)
-        launch_cast_t<FP8_DT_BF16, FP8_E4M3>(x, rows, cols, ldx, bias, q, ldq, qT, ldqT, s);
-    else if (dt == FP8_DT_BF16)
-        launch_cast_t<FP8_DT_BF16, FP8_E5M2>(x, rows, cols, ldx, bias, q, ldq, qT, ldqT, s);
-    else if (fmt == FP8_E4M3)
-        launch_cast_t<FP8_DT_F32, FP8_E4M3>(x, rows, cols, ldx, bias, q, ldq, qT, ldqT, s);
-    else
-        launch_cast_t<FP8_DT_F32, FP8_E5M2>(x, rows, cols, ldx, bias, q, ldq, qT, ldqT, s);
+    with_dt_fmt(dt, fmt, [&](auto D, auto F) {
+        launch_cast_t<decltype(D)::value, decltype(F)::value>(x, rows, cols, ldx, bias, q, ldq, qT, ldqT, s);
+    });
     return hip_status();
 }
 
@@ -556,14 +648,10 @@ int32_t launch_quantise(const void* x, int dt, int64_t rows, int64_t cols, int64
                         int32_t margin, const int32_t* bias_pred, int32_t* bias, uint32_t* amax_bits,
                         uint32_t* flags, uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT,
                         uint32_t* ws, hipStream_t s) {
-    if (dt == FP8_DT_BF16 && fmt == FP8_E4M3)
-        launch_quantise_t<FP8_DT_BF16, FP8_E4M3>(x, rows, cols, ldx, margin, bias_pred, bias, amax_bits, flags, q, ldq, qT, ldqT, ws, s);
-    else if (dt == FP8_DT_BF16)
-        launch_quantise_t<FP8_DT_BF16, FP8_E5M2>(x, rows, cols, ldx, margin, bias_pred, bias, amax_bits, flags, q, ldq, qT, ldqT, ws, s);
-    else if (fmt == FP8_E4M3)
-        launch_quantise_t<FP8_DT_F32, FP8_E4M3>(x, rows, cols, ldx, margin, bias_pred, bias, amax_bits, flags, q, ldq, qT, ldqT, ws, s);
-    else
-        launch_quantise_t<FP8_DT_F32, FP8_E5M2>(x, rows, cols, ldx, margin, bias_pred, bias, amax_bits, flags, q, ldq, qT, ldqT, ws, s);
+    with_dt_fmt(dt, fmt, [&](auto D, auto F) {
+        launch_quantise_t<decltype(D)::value, decltype(F)::value>(x, rows, cols, ldx, margin, bias_pred, bias, amax_bits,
+                                                                  flags, q, ldq, qT, ldqT, ws, s);
+    });
     return hip_status();
 }
 

@@ -9,7 +9,7 @@ namespace {
 
 constexpr int64_t kMaxDim = (int64_t)1 << 40;
 
-bool fmt_ok(int32_t f) { return f == FP8_E4M3 || f == FP8_E5M2; }
+bool fmt_ok(int32_t f) { return f == FP8_E4M3 || f == FP8_E5M2 || f == FP8_E4_A || f == FP8_E5_A; }
 bool dt_ok(int32_t d) { return d == FP8_DT_BF16 || d == FP8_DT_F32; }
 int esize(int32_t d) { return d == FP8_DT_BF16 ? 2 : 4; }
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
@@ -18,7 +18,7 @@ hipStream_t as_stream(void* s) { return (hipStream_t)s; }
 int32_t cast_common(const void* x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx,
                     const int32_t* bias, uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT,
                     int fmt, void* stream) {
-    if (!dt_ok(dt) || rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return FP8_EINVAL;
+    if (!dt_ok(dt) || !fmt_ok(fmt) || rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return FP8_EINVAL;
     if (rows == 0 || cols == 0) return FP8_OK;
     if (!x || !bias || (!q && !qT)) return FP8_EINVAL;
     if (!aligned(x, esize(dt)) || !aligned(bias, 4)) return FP8_EINVAL;
@@ -73,6 +73,12 @@ int32_t fp8_scale_bias(const void* x, int32_t dt, int64_t n, int32_t fmt, int32_
     }
     return launch_scale_bias(x, dt, n, fmt, margin, bias, amax_bits, flags, (uint32_t*)ws,
                              as_stream(stream));
+}
+
+int32_t fp8_cast(const void* x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx, int32_t fmt,
+                 const int32_t* bias, uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT,
+                 void* stream) {
+    return cast_common(x, dt, rows, cols, ldx, bias, q, ldq, qT, ldqT, fmt, stream);
 }
 
 size_t fp8_quantise_ws_bytes(int64_t rows, int64_t cols) {

@@ -18,6 +18,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libfp8lin.so")
 
 E4M3, E5M2 = 0, 1
+E4_A, E5_A = 2, 3   # the paper's formats (Table 7 rows "(a)"); bias and cast calls only
 DT_BF16, DT_F32 = 0, 1
 FLAG_NONFINITE, FLAG_ZERO = 1, 2
 OK, EINVAL, ENOTSUP, EHIP = 0, 1, 2, 3
@@ -25,7 +26,8 @@ OK, EINVAL, ENOTSUP, EHIP = 0, 1, 2, 3
 # Every symbol declared in include/fp8lin.h.
 EXPORTS = (
     "fp8_status_string", "fp8_abi_version", "fp8_scale_bias_ws_bytes", "fp8_scale_bias",
-    "fp8_bias_from_amax", "fp8_cast_e4", "fp8_cast_e5", "fp8_quantise_ws_bytes", "fp8_quantise",
+    "fp8_bias_from_amax", "fp8_cast_e4", "fp8_cast_e5", "fp8_cast", "fp8_quantise_ws_bytes",
+    "fp8_quantise",
     "fp8_linear_fwd", "fp8_linear_bwd_dx",
     "fp8_linear_bwd_dw", "ptq_quantise_weights",
 )
@@ -62,6 +64,8 @@ def lib() -> ctypes.CDLL:
             f = getattr(L, name)
             f.restype = i32
             f.argtypes = [vp, i32, i64, i64, i64, vp, vp, i64, vp, i64, vp]
+        L.fp8_cast.restype = i32
+        L.fp8_cast.argtypes = [vp, i32, i64, i64, i64, i32, vp, vp, i64, vp, i64, vp]
         L.fp8_quantise_ws_bytes.restype = sz
         L.fp8_quantise_ws_bytes.argtypes = [i64, i64]
         L.fp8_quantise.restype = i32
@@ -172,6 +176,21 @@ def fp8_cast_e4(x, bias, q=None, qT=None, want_q=True, want_qT=False, stream=Non
 def fp8_cast_e5(x, bias, q=None, qT=None, want_q=True, want_qT=False, stream=None):
     """Scale by 2^bias and cast to E5M2; returns (q, qT)."""
     return _cast("fp8_cast_e5", x, bias, q, qT, want_q, want_qT, stream)
+
+
+def fp8_cast(x, fmt, bias, q=None, qT=None, want_q=True, want_qT=False, stream=None):
+    """Scale by 2^bias and cast to any of E4M3, E5M2, E4_A, E5_A; returns (q, qT)."""
+    x2 = x if x.dim() == 2 else x.reshape(1, -1)
+    rows, cols = x2.shape
+    if want_q and q is None:
+        q = torch.empty((rows, cols), dtype=torch.uint8, device=x.device)
+    if want_qT and qT is None:
+        qT = torch.empty((cols, rows), dtype=torch.uint8, device=x.device)
+    st = lib().fp8_cast(_p(x2), _dt(x2), rows, cols, _ld(x2), fmt, _p(bias),
+                        _p(q), _ld(q) if q is not None else 0,
+                        _p(qT), _ld(qT) if qT is not None else 0, _stream(stream))
+    _check("fp8_cast", st)
+    return q, qT
 
 
 def fp8_quantise_ws_bytes(rows: int, cols: int) -> int:

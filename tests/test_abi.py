@@ -101,9 +101,17 @@ def test_quantise_rejects(L):
     assert f(FAKE, 0, 4, 8, 8, 0, 0, NULL, FAKE, NULL, NULL, FAKE, 8, NULL, 4, NULL, WS, NULL) == F.EINVAL  # ws
     assert f(FAKE, 0, 4, 8, 8, 0, 0, NULL, FAKE, NULL, NULL, FAKE, 8, NULL, 4, FAKE, 4, NULL) == F.EINVAL   # ws small
     assert f(FAKE, 3, 4, 8, 8, 0, 0, NULL, FAKE, NULL, NULL, FAKE, 8, NULL, 4, FAKE, WS, NULL) == F.EINVAL  # dtype
-    assert f(FAKE, 0, 4, 8, 8, 2, 0, NULL, FAKE, NULL, NULL, FAKE, 8, NULL, 4, FAKE, WS, NULL) == F.EINVAL  # format
+    assert f(FAKE, 0, 4, 8, 8, 4, 0, NULL, FAKE, NULL, NULL, FAKE, 8, NULL, 4, FAKE, WS, NULL) == F.EINVAL  # format
     assert f(FAKE, 0, 4, 8, 8, 0, 1 << 20, NULL, FAKE, NULL, NULL, FAKE, 8, NULL, 4, FAKE, WS, NULL) == F.EINVAL  # margin
     assert f(FAKE, 0, -1, 8, 8, 0, 0, NULL, FAKE, NULL, NULL, FAKE, 8, NULL, 4, FAKE, WS, NULL) == F.EINVAL  # rows < 0
+
+
+def test_generic_cast_rejects(L):
+    f = L.fp8_cast
+    assert f(FAKE, 0, 4, 8, 8, 4, FAKE, FAKE, 8, NULL, 4, NULL) == F.EINVAL    # format
+    assert f(FAKE, 0, 4, 8, 8, -1, FAKE, FAKE, 8, NULL, 4, NULL) == F.EINVAL   # format
+    assert f(FAKE, 0, 4, 8, 8, 2, NULL, FAKE, 8, NULL, 4, NULL) == F.EINVAL    # bias
+    assert f(FAKE, 0, 4, 8, 8, 3, FAKE, NULL, 8, NULL, 4, NULL) == F.EINVAL    # no output
 
 
 def test_gemm_rejects(L):
@@ -127,5 +135,5 @@ def test_ptq_and_bias_from_amax_reject(L):
     assert L.ptq_quantise_weights(FAKE, 0, 4, 4, FAKE, NULL, NULL, NULL, FAKE, 64, NULL) == F.EINVAL
     assert L.ptq_quantise_weights(FAKE, 9, 4, 4, FAKE, NULL, FAKE, NULL, FAKE, 64, NULL) == F.EINVAL
     assert L.fp8_bias_from_amax(NULL, 0, 0, FAKE, NULL, NULL) == F.EINVAL
-    assert L.fp8_bias_from_amax(FAKE, 3, 0, FAKE, NULL, NULL) == F.EINVAL
+    assert L.fp8_bias_from_amax(FAKE, 5, 0, FAKE, NULL, NULL) == F.EINVAL
     assert L.fp8_bias_from_amax(FAKE, 0, 0, ODD, NULL, NULL) == F.EINVAL
