@@ -180,7 +180,7 @@ def measured_traffic(workload: str, kind: str):
     with open(path) as f:
         rec = json.load(f)
     h = hashlib.sha256()
-    for src in ("fp8lin_gemm.hip", "fp8lin_amax_cast.hip"):
+    for src in ("fp8lin_gemm.hip", "fp8lin_amax_cast.hip", "fp8lin_fp8.h"):
         with open(os.path.join(ROOT, "paper_2309_17224_amd", "csrc", src), "rb") as f:
             h.update(f.read())
     if rec.get("kernel_sources_sha256") != h.hexdigest():
