@@ -211,6 +211,37 @@ int32_t fp8_linear_bwd_dx(const uint8_t *dy8, const int32_t *bg, const uint8_t *
                           int64_t K, uint32_t *dx_amax_bits, void *stream);
 
 /*
+ * fp8_linear_fwd_quantise / fp8_linear_bwd_dx_quantise -- the matmul of
+ * fp8_linear_fwd / fp8_linear_bwd_dx (bf16 output) with the amax, Eq. 3 bias
+ * and cast of its output fused into the epilogue, for the next layer that
+ * consumes it (Sec. 3: the bias of a tensor needs its amax before the cast, a
+ * second pass over the output).  Same bits as the matmul followed by
+ * fp8_quantise on its output: the epilogue casts with the predicted bias
+ * while it takes the output's amax; if the exact bias differs, a second kernel
+ * re-casts from the bf16 output it has just written.
+ * y / dx:       out, the bf16 product [M, N] (fwd) / [M, K] (dx), dense.
+ * *_fmt, margin, *_bias_pred, *_bias, *_amax_bits, *_flags: as fp8_quantise
+ *               (bias_pred NULL: the matmul, then a two-pass quantise).
+ * y8 / dx8:     out, codes of the output, row stride ld >= its columns.
+ * y8t / dx8t:   out, optional, the transposed codes, row stride >= its rows.
+ * ws:           workspace of fp8_linear_quantise_ws_bytes(rows, cols) bytes of
+ *               the output, 4-byte aligned; scratch.
+ */
+size_t fp8_linear_quantise_ws_bytes(int64_t rows, int64_t cols);
+int32_t fp8_linear_fwd_quantise(const uint8_t *x8, const int32_t *bx, const uint8_t *w8t,
+                                const int32_t *bw, void *y, int64_t M, int64_t N, int64_t K,
+                                int32_t y_fmt, int32_t margin, const int32_t *y_bias_pred,
+                                int32_t *y_bias, uint32_t *y_amax_bits, uint32_t *y_flags,
+                                uint8_t *y8, int64_t ldy8, uint8_t *y8t, int64_t ldy8t, void *ws,
+                                size_t ws_bytes, void *stream);
+int32_t fp8_linear_bwd_dx_quantise(const uint8_t *dy8, const int32_t *bg, const uint8_t *w8,
+                                   const int32_t *bw, void *dx, int64_t M, int64_t N, int64_t K,
+                                   int32_t dx_fmt, int32_t margin, const int32_t *dx_bias_pred,
+                                   int32_t *dx_bias, uint32_t *dx_amax_bits, uint32_t *dx_flags,
+                                   uint8_t *dx8, int64_t lddx8, uint8_t *dx8t, int64_t lddx8t,
+                                   void *ws, size_t ws_bytes, void *stream);
+
+/*
  * fp8_linear_bwd_dw -- grad-weight FP8 matmul (Sec. 2.2):
  *   dW[k, n] = 2^-(bx + bg) * sum_m X8[m, k] * dY8[m, n]
  * x8t:  [K, M] E4M3 codes: X8 transposed (qT of the activation cast), bias *bx.

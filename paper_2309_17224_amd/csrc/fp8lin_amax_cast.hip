@@ -255,9 +255,10 @@ __global__ __launch_bounds__(kCastThreads) void cast_kernel(
 // the predicted bias (clamped), which block 0 records in *used.
 // Pass 2 (quant_pass2_kernel): every workgroup reduces parts[] and evaluates
 // Eq. 3; block 0 writes bias, amax and flags.  If pass 1 did not cast, or cast
-// with a bias other than the exact one, the workgroups recast all tiles
+// with a bias other than the exact one, the workgroups recast all ncast tiles
 // (grid-stride) with the exact bias; otherwise the codes of pass 1 are already
-// those of the exact bias and nothing more is written.
+// those of the exact bias and nothing more is written.  parts[] may come from
+// another producer of the same tensor (a matmul epilogue) with its own tiling.
 template <int DT, int FMT, bool CAST>
 __global__ __launch_bounds__(kCastThreads) void quant_pass1_kernel(
     const void* __restrict__ x, int64_t rows, int64_t cols, int64_t ldx,
@@ -284,7 +285,7 @@ __global__ __launch_bounds__(kCastThreads) void quant_pass2_kernel(
     const uint32_t* __restrict__ parts, int nparts, const int32_t* __restrict__ used, int have_used,
     int32_t margin, int32_t* __restrict__ bias, uint32_t* __restrict__ amax_bits,
     uint32_t* __restrict__ flags, uint8_t* __restrict__ q, int64_t ldq, uint8_t* __restrict__ qT,
-    int64_t ldqT, int64_t tiles_c, int vec_in, int vec_q, int vec_qT) {
+    int64_t ldqT, int64_t tiles_c, int64_t ncast, int vec_in, int vec_q, int vec_qT) {
     __shared__ __attribute__((aligned(16))) uint8_t tile[kCastCols * kCastRows];
     __shared__ uint32_t red[kCastThreads / 64];
     __shared__ uint32_t amax_s;
@@ -303,7 +304,7 @@ __global__ __launch_bounds__(kCastThreads) void quant_pass2_kernel(
     }
     const int b = clamp_bias(bx);
     if (have_used && *used == b) return;  // pass 1 already wrote these codes
-    for (int64_t t = blockIdx.x; t < nparts; t += gridDim.x)
+    for (int64_t t = blockIdx.x; t < ncast; t += gridDim.x)
         cast_tile<DT, FMT, false>(x, rows, cols, ldx, b, q, ldq, qT, ldqT, t / tiles_c, t % tiles_c,
                                   vec_in, vec_q, vec_qT, tile);
 }
@@ -348,7 +349,24 @@ void launch_quantise_t(const void* x, int64_t rows, int64_t cols, int64_t ldx, i
     const int nb2 = (int)(ntiles < kQuantPass2MaxBlocks ? ntiles : kQuantPass2MaxBlocks);
     hipLaunchKernelGGL((quant_pass2_kernel<DT, FMT>), dim3(nb2), dim3(kCastThreads), 0, s, x, rows, cols, ldx,
                        parts, (int)ntiles, used, bias_pred ? 1 : 0, margin, bias, amax_bits, flags, q, ldq,
-                       qT, ldqT, tiles_c, vec_in, vec_q, vec_qT);
+                       qT, ldqT, tiles_c, ntiles, vec_in, vec_q, vec_qT);
+}
+
+template <int DT, int FMT>
+void launch_quant_check_t(const void* x, int64_t rows, int64_t cols, int64_t ldx, int32_t margin,
+                          const uint32_t* parts, int nparts, const int32_t* used, int32_t* bias,
+                          uint32_t* amax_bits, uint32_t* flags, uint8_t* q, int64_t ldq, uint8_t* qT,
+                          int64_t ldqT, hipStream_t s) {
+    const int64_t tiles_c = (cols + kCastCols - 1) / kCastCols;
+    const int64_t ncast = ((rows + kCastRows - 1) / kCastRows) * tiles_c;
+    const int esz = DT == FP8_DT_BF16 ? 2 : 4;
+    const int vec_in = ((uintptr_t)x % 16 == 0) && ((ldx * esz) % 16 == 0);
+    const int vec_q = q && ((uintptr_t)q % 8 == 0) && (ldq % 8 == 0);
+    const int vec_qT = qT && ((uintptr_t)qT % 16 == 0) && (ldqT % 16 == 0);
+    const int nb2 = (int)(ncast < kQuantPass2MaxBlocks ? ncast : kQuantPass2MaxBlocks);
+    hipLaunchKernelGGL((quant_pass2_kernel<DT, FMT>), dim3(nb2), dim3(kCastThreads), 0, s, x, rows, cols, ldx,
+                       parts, nparts, used, 1, margin, bias, amax_bits, flags, q, ldq, qT, ldqT, tiles_c, ncast,
+                       vec_in, vec_q, vec_qT);
 }
 
 // Host dispatch of (element type, format) to kernel template arguments.
@@ -411,6 +429,17 @@ int32_t launch_cast(const void* x, int dt, int64_t rows, int64_t cols, int64_t l
                     hipStream_t s) {
     with_dt_fmt(dt, fmt, [&](auto D, auto F) {
         launch_cast_t<decltype(D)::value, decltype(F)::value>(x, rows, cols, ldx, bias, q, ldq, qT, ldqT, s);
+    });
+    return hip_status();
+}
+
+int32_t launch_quant_check(const void* x, int dt, int64_t rows, int64_t cols, int64_t ldx, int fmt,
+                           int32_t margin, const uint32_t* parts, int nparts, const int32_t* used,
+                           int32_t* bias, uint32_t* amax_bits, uint32_t* flags, uint8_t* q, int64_t ldq,
+                           uint8_t* qT, int64_t ldqT, hipStream_t s) {
+    with_dt_fmt(dt, fmt, [&](auto D, auto F) {
+        launch_quant_check_t<decltype(D)::value, decltype(F)::value>(x, rows, cols, ldx, margin, parts, nparts, used,
+                                                                     bias, amax_bits, flags, q, ldq, qT, ldqT, s);
     });
     return hip_status();
 }

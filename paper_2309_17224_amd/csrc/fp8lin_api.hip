@@ -148,6 +148,60 @@ int32_t fp8_linear_bwd_dw(const uint8_t* x8t, const int32_t* bx, const uint8_t* 
     return gemm_common(x8t, FP8_E4M3, bx, dy8t, FP8_E5M2, bg, dw, dw_dt, K, N, M, nullptr, stream);
 }
 
+size_t fp8_linear_quantise_ws_bytes(int64_t M, int64_t N) {
+    if (M <= 0 || N <= 0 || M > kMaxDim || N > kMaxDim) return 0;
+    return (size_t)gemm_quantise_ws_words(M, N) * sizeof(uint32_t);
+}
+
+namespace {
+// C [rows, cols] (bf16) = 2^-(*ba + *bb) A [rows, kc] . B [cols, kc]^T, then
+// its bias and codes (see fp8_linear_fwd_quantise).
+int32_t gemm_quantise_common(const uint8_t* a, int fa, const int32_t* ba, const uint8_t* b,
+                             const int32_t* bb, void* c, int64_t rows, int64_t cols, int64_t kc,
+                             int32_t fmt, int32_t margin, const int32_t* pred, int32_t* bias,
+                             uint32_t* amax_bits, uint32_t* flags, uint8_t* q, int64_t ldq, uint8_t* qT,
+                             int64_t ldqT, void* ws, size_t ws_bytes, void* stream) {
+    if (!fmt_ok(fmt) || rows < 0 || cols < 0 || kc < 0 || rows > kMaxDim || cols > kMaxDim || kc > kMaxDim)
+        return FP8_EINVAL;
+    if (margin < -FP8_MAX_MARGIN || margin > FP8_MAX_MARGIN) return FP8_EINVAL;
+    if (!bias || !aligned(bias, 4) || (pred && !aligned(pred, 4))) return FP8_EINVAL;
+    if ((amax_bits && !aligned(amax_bits, 4)) || (flags && !aligned(flags, 4))) return FP8_EINVAL;
+    if (rows == 0 || cols == 0)
+        return launch_scale_bias(nullptr, FP8_DT_BF16, 0, fmt, margin, bias, amax_bits, flags, nullptr,
+                                 as_stream(stream));
+    if (!c || !ba || !bb || !q || (kc > 0 && (!a || !b)) || !ws) return FP8_EINVAL;
+    if (!aligned(c, 2) || !aligned(ba, 4) || !aligned(bb, 4) || !aligned(ws, 4)) return FP8_EINVAL;
+    if (ldq < cols || (qT && ldqT < rows)) return FP8_EINVAL;
+    if (ws_bytes < fp8_linear_quantise_ws_bytes(rows, cols)) return FP8_EINVAL;
+    if (rows > INT32_MAX || cols > INT32_MAX) return FP8_ENOTSUP;
+    return launch_gemm_nt_quantise(a, fa, ba, b, FP8_E4M3, bb, c, rows, cols, kc, fmt, margin, pred, bias,
+                                   amax_bits, flags, q, ldq, qT, ldqT, (uint32_t*)ws, as_stream(stream));
+}
+}  // namespace
+
+int32_t fp8_linear_fwd_quantise(const uint8_t* x8, const int32_t* bx, const uint8_t* w8t,
+                                const int32_t* bw, void* y, int64_t M, int64_t N, int64_t K,
+                                int32_t y_fmt, int32_t margin, const int32_t* y_bias_pred,
+                                int32_t* y_bias, uint32_t* y_amax_bits, uint32_t* y_flags,
+                                uint8_t* y8, int64_t ldy8, uint8_t* y8t, int64_t ldy8t, void* ws,
+                                size_t ws_bytes, void* stream) {
+    return gemm_quantise_common(x8, FP8_E4M3, bx, w8t, bw, y, M, N, K, y_fmt, margin, y_bias_pred,
+                                y_bias, y_amax_bits, y_flags, y8, ldy8, y8t, ldy8t, ws, ws_bytes,
+                                stream);
+}
+
+int32_t fp8_linear_bwd_dx_quantise(const uint8_t* dy8, const int32_t* bg, const uint8_t* w8,
+                                   const int32_t* bw, void* dx, int64_t M, int64_t N, int64_t K,
+                                   int32_t dx_fmt, int32_t margin, const int32_t* dx_bias_pred,
+                                   int32_t* dx_bias, uint32_t* dx_amax_bits, uint32_t* dx_flags,
+                                   uint8_t* dx8, int64_t lddx8, uint8_t* dx8t, int64_t lddx8t,
+                                   void* ws, size_t ws_bytes, void* stream) {
+    // dX [M, K] = dY8 [M, N] . W8 [K, N]^T: contraction over N.
+    return gemm_quantise_common(dy8, FP8_E5M2, bg, w8, bw, dx, M, K, N, dx_fmt, margin, dx_bias_pred,
+                                dx_bias, dx_amax_bits, dx_flags, dx8, lddx8, dx8t, lddx8t, ws, ws_bytes,
+                                stream);
+}
+
 int32_t ptq_quantise_weights(const void* w, int32_t dt, int64_t K, int64_t N, uint8_t* w8,
                              uint8_t* w8t, int32_t* bw, uint32_t* flags, void* ws, size_t ws_bytes,
                              void* stream) {

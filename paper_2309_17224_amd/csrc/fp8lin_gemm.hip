@@ -35,6 +35,7 @@
 // Decode kernel (M <= 32): weight-streaming split-K, see below.
 // Fallback kernel (any K or alignment): 64 x 64 tiles, byte loads with
 // bounds checks and zero fill, same MFMA and epilogue.
+#include "fp8lin_fp8.h"
 #include "fp8lin_internal.h"
 
 namespace fp8lin {
@@ -169,14 +170,32 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
 }
 
+__device__ __forceinline__ int bq_used(const int32_t* pred) { return clamp_bias(*pred); }
+
 // Epilogue staging rows (bytes): 32 output rows of a wave per pass.
 constexpr int kEpRowBf16 = 128 * 2 + 16, kEpRowF32 = 128 * 4 + 16;
 
-template <int FA, int FB, int OUT_DT, bool AMAX>
+// Output codes of the fused quantise (QF >= 0, bf16 output only): Y8 [M, N]
+// and optionally Y8T [N, M] in format QF, cast with a predicted bias; the
+// tile maxima and the prediction used go to a workspace for the exact-bias
+// check (see launch_gemm_nt_quantise).
+struct QuantOut {
+    const int32_t* pred;  // predicted bias (device)
+    int32_t* used;        // out: the clamped prediction the codes were cast with
+    uint32_t* parts;      // out: per-workgroup largest |Y| pattern (bf16 bits)
+    uint8_t* y8;
+    int64_t ldy8;
+    uint8_t* y8t;  // may be null
+    int64_t ldy8t;
+    int vec8, vec8t;  // 16-byte stores allowed
+};
+
+template <int FA, int FB, int OUT_DT, bool AMAX, int QF = -1>
 __global__ __launch_bounds__(kThreads) void gemm_nt_256(
     const uint8_t* __restrict__ A, const uint8_t* __restrict__ B, const int32_t* __restrict__ ba_p,
     const int32_t* __restrict__ bb_p, void* __restrict__ C, int M, int N, int K, int tiles_m,
-    int tiles_n, int vec_out, uint32_t* __restrict__ amax_out) {
+    int tiles_n, int vec_out, uint32_t* __restrict__ amax_out, QuantOut qo) {
+    static_assert(QF < 0 || OUT_DT == FP8_DT_BF16, "fused quantise is for bf16 outputs");
     __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * 2 * kTileBytes];
 
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -274,6 +293,12 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_256(
         uint8_t* ep = smem + w * 32 * kEpRowBf16;
         typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
         u16x2 m2 = {0, 0};
+        // Fused quantise: the codes of the tile, row-major, in the upper 64 KiB
+        // (row r = 256 bytes; 16-byte chunk c stored at chunk c ^ (r % 16)).
+        uint8_t* cs = smem + 2 * kTileBytes;
+        int bq = 0;
+        uint32_t codes[8][8];
+        if (QF >= 0) bq = clamp_bias(*qo.pred);
 #pragma unroll
         for (int i2 = 0; i2 < 4; ++i2) {
 #pragma unroll
@@ -283,9 +308,19 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_256(
                 for (int j = 0; j < 8; ++j) {
                     const uint32_t lo = pack_bf16x2(ldexpf(acc[i][j][0], sh), ldexpf(acc[i][j][1], sh));
                     const uint32_t hi = pack_bf16x2(ldexpf(acc[i][j][2], sh), ldexpf(acc[i][j][3], sh));
-                    if (AMAX) {
+                    if (AMAX || QF >= 0) {
                         m2 = __builtin_elementwise_max(m2, __builtin_bit_cast(u16x2, lo & 0x7FFF7FFFu));
                         m2 = __builtin_elementwise_max(m2, __builtin_bit_cast(u16x2, hi & 0x7FFF7FFFu));
+                    }
+                    if (QF >= 0) {
+                        uint32_t c4 = cast4_bf16<QF < 0 ? 0 : QF>(lo, hi, bq);
+                        if (__builtin_expect(any_nan_bf16(lo, hi), 0)) {
+                            const uint32_t hs[4] = {lo & 0xFFFFu, lo >> 16, hi & 0xFFFFu, hi >> 16};
+                            c4 = nan_patch<QF < 0 ? 0 : QF>(c4, hs);
+                        }
+                        codes[i][j] = c4;
+                        const int r = wm * 128 + i * 16 + frow, col = wn * 128 + j * 16 + 4 * fg;
+                        *(uint32_t*)(cs + r * 256 + ((((col >> 4) ^ r) & 15) << 4) + (col & 15)) = c4;
                     }
                     *(uint2*)(ep + (ii * 16 + frow) * kEpRowBf16 + (j * 16 + 4 * fg) * 2) = make_uint2(lo, hi);
                 }
@@ -307,6 +342,57 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_256(
             }
         }
         mx = (uint32_t)max(m2.x, m2.y) << 16;
+        if (QF >= 0) {
+            // Y8 rows from the staged codes: 4096 chunks of 16 bytes, 16 per thread.
+            __syncthreads();
+#pragma unroll
+            for (int h = 0; h < 16; ++h) {
+                const int idx = threadIdx.x + h * kThreads, r = idx >> 4, c = idx & 15;
+                const uint4 v = *(const uint4*)(cs + r * 256 + (((c ^ r) & 15) << 4));
+                const int64_t m = m0 + r, n = n0 + c * 16;
+                if (m < M && n < N) {
+                    uint8_t* p = qo.y8 + m * qo.ldy8 + n;
+                    if (qo.vec8 && n + 16 <= N) {
+                        *(uint4*)p = v;
+                    } else {
+                        const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+                        for (int e = 0; e < 16 && n + e < N; ++e) p[e] = (uint8_t)(wv[e >> 2] >> (8 * (e & 3)));
+                    }
+                }
+            }
+            if (qo.y8t) {
+                // Y8T: restage the codes column-major (column c = 256 bytes of
+                // rows; chunk q of column c stored at chunk q ^ (c % 16)).
+                __syncthreads();
+#pragma unroll
+                for (int i = 0; i < 8; ++i)
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        const int r = wm * 128 + i * 16 + frow, col0 = wn * 128 + j * 16 + 4 * fg;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const int c = col0 + e;
+                            cs[c * 256 + ((((r >> 4) ^ c) & 15) << 4) + (r & 15)] = (uint8_t)(codes[i][j] >> (8 * e));
+                        }
+                    }
+                __syncthreads();
+#pragma unroll
+                for (int h = 0; h < 16; ++h) {
+                    const int idx = threadIdx.x + h * kThreads, c = idx >> 4, q = idx & 15;
+                    const uint4 v = *(const uint4*)(cs + c * 256 + (((q ^ c) & 15) << 4));
+                    const int64_t n = n0 + c, m = m0 + q * 16;
+                    if (n < N && m < M) {
+                        uint8_t* p = qo.y8t + n * qo.ldy8t + m;
+                        if (qo.vec8t && m + 16 <= M) {
+                            *(uint4*)p = v;
+                        } else {
+                            const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+                            for (int e = 0; e < 16 && m + e < M; ++e) p[e] = (uint8_t)(wv[e >> 2] >> (8 * (e & 3)));
+                        }
+                    }
+                }
+            }
+        }
     } else {
         uint8_t* ep = smem + w * 32 * kEpRowF32;
 #pragma unroll
@@ -348,6 +434,16 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_256(
         // so including them cannot change the maximum
         mx = wave_max_u32(mx);
         if (lane == 0) atomicMax(amax_out, mx);
+    }
+    if (QF >= 0) {  // this workgroup's largest |Y| (bf16 magnitude pattern)
+        __shared__ uint32_t wmx[kThreads / 64];
+        const uint32_t m16 = wave_max_u32(mx >> 16);
+        if (lane == 0) wmx[w] = m16;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            qo.parts[blockIdx.x] = max(max(wmx[0], wmx[1]), max(wmx[2], wmx[3]));
+            if (blockIdx.x == 0) *qo.used = bq_used(qo.pred);
+        }
     }
 }
 
@@ -555,7 +651,7 @@ void launch_t(const uint8_t* A, const int32_t* ba, const uint8_t* B, const int32
         const int tiles_m = (int)((M + kBM - 1) / kBM), tiles_n = (int)((N + kBN - 1) / kBN);
         const int vec16 = ((uintptr_t)C % 16 == 0) && ((N * esz) % 16 == 0);
         hipLaunchKernelGGL((gemm_nt_256<FA, FB, OUT_DT, AMAX>), dim3(tiles_m * tiles_n), dim3(kThreads), 0,
-                           s, A, B, ba, bb, C, (int)M, (int)N, (int)K, tiles_m, tiles_n, vec16, amax);
+                           s, A, B, ba, bb, C, (int)M, (int)N, (int)K, tiles_m, tiles_n, vec16, amax, QuantOut{});
     } else {
         const int64_t tiles_m = (M + kSBM - 1) / kSBM, tiles_n = (N + kSBN - 1) / kSBN;
         hipLaunchKernelGGL((gemm_nt_small<FA, FB, OUT_DT, AMAX>), dim3((unsigned)(tiles_m * tiles_n)),
@@ -575,7 +671,68 @@ void dispatch_out(const uint8_t* A, const int32_t* ba, const uint8_t* B, const i
     }
 }
 
+template <int FA, int FB, int QF>
+void launch_fused_t(const uint8_t* A, const int32_t* ba, const uint8_t* B, const int32_t* bb, void* C,
+                    int64_t M, int64_t N, int64_t K, const QuantOut& qo, hipStream_t s) {
+    const int tiles_m = (int)((M + kBM - 1) / kBM), tiles_n = (int)((N + kBN - 1) / kBN);
+    const int vec16 = ((uintptr_t)C % 16 == 0) && ((N * 2) % 16 == 0);
+    hipLaunchKernelGGL((gemm_nt_256<FA, FB, FP8_DT_BF16, false, QF>), dim3(tiles_m * tiles_n), dim3(kThreads), 0,
+                       s, A, B, ba, bb, C, (int)M, (int)N, (int)K, tiles_m, tiles_n, vec16, nullptr, qo);
+}
+
+template <int FA, int FB>
+void fused_fmt(int qfmt, const uint8_t* A, const int32_t* ba, const uint8_t* B, const int32_t* bb, void* C,
+               int64_t M, int64_t N, int64_t K, const QuantOut& qo, hipStream_t s) {
+    switch (qfmt) {
+        case FP8_E4M3: launch_fused_t<FA, FB, FP8_E4M3>(A, ba, B, bb, C, M, N, K, qo, s); break;
+        case FP8_E5M2: launch_fused_t<FA, FB, FP8_E5M2>(A, ba, B, bb, C, M, N, K, qo, s); break;
+        case FP8_E4_A: launch_fused_t<FA, FB, FP8_E4_A>(A, ba, B, bb, C, M, N, K, qo, s); break;
+        default: launch_fused_t<FA, FB, FP8_E5_A>(A, ba, B, bb, C, M, N, K, qo, s); break;
+    }
+}
+
 }  // namespace
+
+int64_t gemm_quantise_ws_words(int64_t M, int64_t N) {
+    const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
+    const int64_t q = quantise_ws_words(M, N);
+    return 1 + tiles > q ? 1 + tiles : q;
+}
+
+int32_t launch_gemm_nt_quantise(const uint8_t* A, int fa, const int32_t* ba, const uint8_t* B, int fb,
+                                const int32_t* bb, void* C, int64_t M, int64_t N, int64_t K, int qfmt,
+                                int32_t margin, const int32_t* pred, int32_t* bias, uint32_t* amax_bits,
+                                uint32_t* flags, uint8_t* y8, int64_t ldy8, uint8_t* y8t, int64_t ldy8t,
+                                uint32_t* ws, hipStream_t s) {
+    const bool fused = pred && (K % kBK == 0) && ((uintptr_t)A % 16 == 0) && ((uintptr_t)B % 16 == 0) && M > 32 &&
+                       M <= INT32_MAX && N <= INT32_MAX && K < (1 << 22) && (fa == FP8_E4M3 || fa == FP8_E5M2) &&
+                       fb == FP8_E4M3;
+    if (!fused) {  // matmul, then the quantise of its output (same bits, more passes)
+        const int32_t st = launch_gemm_nt(A, fa, ba, B, fb, bb, C, FP8_DT_BF16, M, N, K, nullptr, s);
+        if (st != FP8_OK) return st;
+        return launch_quantise(C, FP8_DT_BF16, M, N, N, qfmt, margin, pred, bias, amax_bits, flags, y8, ldy8, y8t,
+                               ldy8t, ws, s);
+    }
+    QuantOut qo;
+    qo.pred = pred;
+    qo.used = (int32_t*)ws;
+    qo.parts = ws + 1;
+    qo.y8 = y8;
+    qo.ldy8 = ldy8;
+    qo.y8t = y8t;
+    qo.ldy8t = ldy8t;
+    qo.vec8 = ((uintptr_t)y8 % 16 == 0) && (ldy8 % 16 == 0);
+    qo.vec8t = y8t && ((uintptr_t)y8t % 16 == 0) && (ldy8t % 16 == 0);
+    if (fa == FP8_E4M3)
+        fused_fmt<FP8_E4M3, FP8_E4M3>(qfmt, A, ba, B, bb, C, M, N, K, qo, s);
+    else
+        fused_fmt<FP8_E5M2, FP8_E4M3>(qfmt, A, ba, B, bb, C, M, N, K, qo, s);
+    const int tiles = (int)(((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN));
+    const int32_t st = hip_status();
+    if (st != FP8_OK) return st;
+    return launch_quant_check(C, FP8_DT_BF16, M, N, N, qfmt, margin, ws + 1, tiles, (int32_t*)ws, bias, amax_bits,
+                              flags, y8, ldy8, y8t, ldy8t, s);
+}
 
 int32_t launch_gemm_nt(const uint8_t* A, int fa, const int32_t* ba, const uint8_t* B, int fb,
                        const int32_t* bb, void* C, int out_dt, int64_t M, int64_t N, int64_t K,

@@ -33,6 +33,25 @@ int32_t launch_quantise(const void* x, int dt, int64_t rows, int64_t cols, int64
                         uint32_t* flags, uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT,
                         uint32_t* ws, hipStream_t s);
 
+// The exact-bias check and recast of fp8_quantise's second pass for a tensor
+// x whose per-tile maxima (nparts of them, any tiling) and the prediction its
+// codes were cast with (*used) were written by another kernel.
+int32_t launch_quant_check(const void* x, int dt, int64_t rows, int64_t cols, int64_t ldx, int fmt,
+                           int32_t margin, const uint32_t* parts, int nparts, const int32_t* used,
+                           int32_t* bias, uint32_t* amax_bits, uint32_t* flags, uint8_t* q, int64_t ldq,
+                           uint8_t* qT, int64_t ldqT, hipStream_t s);
+
+// Matmul with bf16 output C whose epilogue also casts C to format qfmt with
+// the predicted bias *pred and writes y8 (and y8t if non-null), followed by
+// the exact-bias check: the same bits as launch_gemm_nt followed by
+// launch_quantise.  ws holds gemm_quantise_ws_words(M, N) uint32 words.
+int64_t gemm_quantise_ws_words(int64_t M, int64_t N);
+int32_t launch_gemm_nt_quantise(const uint8_t* A, int fa, const int32_t* ba, const uint8_t* B, int fb,
+                                const int32_t* bb, void* C, int64_t M, int64_t N, int64_t K, int qfmt,
+                                int32_t margin, const int32_t* pred, int32_t* bias, uint32_t* amax_bits,
+                                uint32_t* flags, uint8_t* y8, int64_t ldy8, uint8_t* y8t, int64_t ldy8t,
+                                uint32_t* ws, hipStream_t s);
+
 // C[m, n] = 2^-(*ba + *bb) * sum_k A[m, k] * B[n, k]; A [M, K] (format fa),
 // B [N, K] (format fb), both dense; C [M, N] dense of type out_dt.
 int32_t launch_gemm_nt(const uint8_t* A, int fa, const int32_t* ba, const uint8_t* B, int fb,

@@ -28,7 +28,8 @@ EXPORTS = (
     "fp8_status_string", "fp8_abi_version", "fp8_scale_bias_ws_bytes", "fp8_scale_bias",
     "fp8_bias_from_amax", "fp8_cast_e4", "fp8_cast_e5", "fp8_cast", "fp8_quantise_ws_bytes",
     "fp8_quantise",
-    "fp8_linear_fwd", "fp8_linear_bwd_dx",
+    "fp8_linear_fwd", "fp8_linear_bwd_dx", "fp8_linear_quantise_ws_bytes",
+    "fp8_linear_fwd_quantise", "fp8_linear_bwd_dx_quantise",
     "fp8_linear_bwd_dw", "ptq_quantise_weights",
 )
 
@@ -75,6 +76,13 @@ def lib() -> ctypes.CDLL:
             f = getattr(L, name)
             f.restype = i32
             f.argtypes = [vp, vp, vp, vp, vp, i32, i64, i64, i64, vp, vp]
+        L.fp8_linear_quantise_ws_bytes.restype = sz
+        L.fp8_linear_quantise_ws_bytes.argtypes = [i64, i64]
+        for name in ("fp8_linear_fwd_quantise", "fp8_linear_bwd_dx_quantise"):
+            f = getattr(L, name)
+            f.restype = i32
+            f.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i32, i32, vp, vp, vp, vp, vp, i64, vp,
+                          i64, vp, sz, vp]
         L.fp8_linear_bwd_dw.restype = i32
         L.fp8_linear_bwd_dw.argtypes = [vp, vp, vp, vp, vp, i32, i64, i64, i64, vp]
         L.ptq_quantise_weights.restype = i32
@@ -258,6 +266,50 @@ def fp8_linear_bwd_dx(dy8, bg, w8, bw, out_dt=DT_BF16, dx=None, dx_amax_bits=Non
                                  _p(dx_amax_bits), _stream(stream))
     _check("fp8_linear_bwd_dx", st)
     return dx
+
+
+def _gemm_quantise(name, a8, ba, b8, bb, out, rows, cols, kc, fmt, margin, bias_pred, bias,
+                   amax_bits, flags, q, qT, want_qT, ws, stream):
+    dev = a8.device
+    out = _out((rows, cols), DT_BF16, dev, out)
+    bias = _i32(dev) if bias is None else bias
+    amax_bits = _i32(dev) if amax_bits is None else amax_bits
+    flags = _i32(dev) if flags is None else flags
+    if q is None:
+        q = torch.empty((rows, cols), dtype=torch.uint8, device=dev)
+    if want_qT and qT is None:
+        qT = torch.empty((cols, rows), dtype=torch.uint8, device=dev)
+    if ws is None:
+        ws = torch.empty(max(int(lib().fp8_linear_quantise_ws_bytes(rows, cols)), 4), dtype=torch.uint8,
+                         device=dev)
+    st = getattr(lib(), name)(_p(a8), _p(ba), _p(b8), _p(bb), _p(out), *(
+        (rows, cols, kc) if name == "fp8_linear_fwd_quantise" else (rows, kc, cols)),
+        fmt, margin, _p(bias_pred), _p(bias), _p(amax_bits), _p(flags), _p(q), _ld(q), _p(qT),
+        _ld(qT) if qT is not None else 0, _p(ws), ws.numel() * ws.element_size(), _stream(stream))
+    _check(name, st)
+    return out, q, qT, bias, amax_bits, flags
+
+
+def fp8_linear_fwd_quantise(x8, bx, w8t, bw, fmt=E4M3, margin=0, bias_pred=None, y=None, bias=None,
+                            amax_bits=None, flags=None, y8=None, y8t=None, want_y8t=False, ws=None,
+                            stream=None):
+    """Y = fp8_linear_fwd(...) (bf16) and its FP8 codes, bias, amax, flags from
+    the epilogue.  Returns (y, y8, y8t, bias, amax_bits, flags)."""
+    M, K = x8.shape
+    N = w8t.shape[0]
+    return _gemm_quantise("fp8_linear_fwd_quantise", x8, bx, w8t, bw, y, M, N, K, fmt, margin,
+                          bias_pred, bias, amax_bits, flags, y8, y8t, want_y8t, ws, stream)
+
+
+def fp8_linear_bwd_dx_quantise(dy8, bg, w8, bw, fmt=E5M2, margin=0, bias_pred=None, dx=None,
+                               bias=None, amax_bits=None, flags=None, dx8=None, dx8t=None,
+                               want_dx8t=False, ws=None, stream=None):
+    """dX = fp8_linear_bwd_dx(...) (bf16) and its FP8 codes etc.  Returns
+    (dx, dx8, dx8t, bias, amax_bits, flags)."""
+    M, N = dy8.shape
+    K = w8.shape[0]
+    return _gemm_quantise("fp8_linear_bwd_dx_quantise", dy8, bg, w8, bw, dx, M, K, N, fmt, margin,
+                          bias_pred, bias, amax_bits, flags, dx8, dx8t, want_dx8t, ws, stream)
 
 
 def fp8_linear_bwd_dw(x8t, bx, dy8t, bg, out_dt=DT_F32, dw=None, stream=None):
