@@ -46,7 +46,8 @@ __global__ __launch_bounds__(kAmaxThreads) void amax_partial_kernel(const void* 
         if (DT == FP8_DT_BF16) {
             us2 mm = {0, 0};
             for (; i + 3 * nth < nv; i += 4 * nth) {
-                const uint4 a = p[i], b = p[i + nth], c = p[i + 2 * nth], d = p[i + 3 * nth];
+                const uint4 a = ld_stream(p + i), b = ld_stream(p + i + nth), c = ld_stream(p + i + 2 * nth),
+                            d = ld_stream(p + i + 3 * nth);
                 mm = fold_bf16(mm, a);
                 mm = fold_bf16(mm, b);
                 mm = fold_bf16(mm, c);
@@ -56,7 +57,8 @@ __global__ __launch_bounds__(kAmaxThreads) void amax_partial_kernel(const void* 
             m = max((uint32_t)mm.x, (uint32_t)mm.y);
         } else {
             for (; i + 3 * nth < nv; i += 4 * nth) {
-                const uint4 a = p[i], b = p[i + nth], c = p[i + 2 * nth], d = p[i + 3 * nth];
+                const uint4 a = ld_stream(p + i), b = ld_stream(p + i + nth), c = ld_stream(p + i + 2 * nth),
+                            d = ld_stream(p + i + 3 * nth);
                 m = fold_f32(m, a);
                 m = fold_f32(m, b);
                 m = fold_f32(m, c);
@@ -132,7 +134,7 @@ __device__ __forceinline__ uint32_t cast_tile(const void* __restrict__ x, int64_
         if (DT == FP8_DT_BF16) {
             uint4 v[kRpt];
 #pragma unroll
-            for (int i = 0; i < kRpt; ++i) v[i] = *(const uint4*)((const uint16_t*)x + (r0 + i) * ldx + c0);
+            for (int i = 0; i < kRpt; ++i) v[i] = ld_stream((const uint16_t*)x + (r0 + i) * ldx + c0);
             if (MAX) {
                 us2 mm = {0, 0};
 #pragma unroll
@@ -154,7 +156,7 @@ __device__ __forceinline__ uint32_t cast_tile(const void* __restrict__ x, int64_
 #pragma unroll
             for (int i = 0; i < kRpt; ++i) {
                 const uint4* p = (const uint4*)((const uint32_t*)x + (r0 + i) * ldx + c0);
-                const uint4 a = p[0], bb = p[1];
+                const uint4 a = ld_stream(p), bb = ld_stream(p + 1);
                 if (MAX) mag = fold_f32(fold_f32(mag, a), bb);
                 lo[i] = cast4_f32<FMT>(a, b);
                 hi[i] = cast4_f32<FMT>(bb, b);

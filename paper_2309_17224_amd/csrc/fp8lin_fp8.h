@@ -236,6 +236,14 @@ __device__ __forceinline__ uint32_t cast1(const void* x, int64_t idx, int b) {
     return c;
 }
 
+// 16-byte load of input data read once per pass, with the non-temporal hint
+// (streaming reads from HBM run about 7-10 % faster with it).
+__device__ __forceinline__ uint4 ld_stream(const void* p) {
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 v = __builtin_nontemporal_load((const u32x4*)p);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // Biases beyond this saturate or flush every input; casts clamp to it.
 __device__ __forceinline__ int clamp_bias(int32_t b) { return max(-kBiasClamp, min(kBiasClamp, b)); }
 
