@@ -172,6 +172,13 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
 
 __device__ __forceinline__ int bq_used(const int32_t* pred) { return clamp_bias(*pred); }
 
+// 16-byte store of matmul output with the non-temporal hint: the output is not
+// read again by this kernel and should not displace cached operands.
+__device__ __forceinline__ void st_stream(void* p, uint4 v) {
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w}, (u32x4*)p);
+}
+
 // Epilogue staging rows (bytes): 32 output rows of a wave per pass.
 constexpr int kEpRowBf16 = 128 * 2 + 16, kEpRowF32 = 128 * 4 + 16;
 
@@ -333,7 +340,7 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_256(
                 if (m < M) {
                     uint16_t* p = (uint16_t*)C + m * N + n;
                     if (vec_out && n + 8 <= N) {
-                        *(uint4*)p = v;
+                        st_stream(p, v);
                     } else {
                         const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
                         for (int e = 0; e < 8 && n + e < N; ++e) p[e] = (uint16_t)(wv[e >> 1] >> (16 * (e & 1)));
@@ -420,7 +427,7 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_256(
                 if (m < M) {
                     float* p = (float*)C + m * N + n;
                     if (vec_out && n + 4 <= N) {
-                        *(float4*)p = v;
+                        st_stream(p, make_uint4(__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)));
                     } else {
                         const float fv[4] = {v.x, v.y, v.z, v.w};
                         for (int e = 0; e < 4 && n + e < N; ++e) p[e] = fv[e];
