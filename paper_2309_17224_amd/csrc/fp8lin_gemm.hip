@@ -7,13 +7,20 @@
 // this form once the casts have written the transposed copies they need.
 //
 // Main kernel (K a multiple of 128, 16-byte aligned operands):
-//  * 256 x 256 output tile per workgroup of 4 waves; each wave owns a
-//    128 x 128 sub-tile = 8 x 8 blocks of v_mfma_f32_16x16x128_f8f6f4.
+//  * 256 x 256 output tile per workgroup of 8 waves, two per SIMD (wave w
+//    runs on SIMD w % 4).  Each wave owns a 64 x 128 sub-tile = 4 x 8 blocks
+//    of v_mfma_f32_16x16x128_f8f6f4; the two waves of a SIMD own the two
+//    halves of one 128 x 128 quadrant.
 //  * K advances 128 bytes at a time; both operand tiles (256 rows x 128 B)
 //    go HBM/L2 -> LDS with global_load_lds_dwordx4 (no VGPR staging) into a
-//    double buffer (2 x 64 KiB), so loads of step k+1 overlap the MFMAs of
-//    step k; the copies are spread between MFMAs and one barrier per step
-//    orders both buffers (see the main loop).
+//    double buffer (2 x 64 KiB).
+//  * The two waves of a SIMD alternate between an MFMA phase and a load
+//    phase, the phases separated by workgroup barriers: while one issues its
+//    32 MFMAs of step k, the other reads all its fragments of its next step
+//    into registers (and, in group 0, issues the copies of a later step).
+//    The matrix core of each SIMD is fed by one wave at a time, and the
+//    cost of issuing vector-memory and LDS instructions falls on the wave
+//    that is not feeding it (see the main loop).
 //  * LDS rows are 128 B; the 16-byte chunk index is XOR-swizzled with the row
 //    (chunk ^ chunk_swz(row), below) by choosing which global chunk each lane
 //    fetches.  The LDS has 64 four-byte banks (16 groups of 16 bytes) and
@@ -72,6 +79,17 @@ template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
     static_assert(N >= 0 && N < 64, "vmcnt range");
     asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
+// Wait until every LDS read of this wave has returned its data.
+__device__ __forceinline__ void wait_lgkmcnt0() { asm volatile("s_waitcnt lgkmcnt(0)" : : : "memory"); }
+
+// Workgroup barrier with no memory fence: the main loop orders its LDS
+// traffic itself (wait_vmcnt for the copies, wait_lgkmcnt0 for the reads).
+__device__ __forceinline__ void ws_barrier() {
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
 }
 
 // The two 16-byte pieces of an MFMA operand fragment, as one 8-register vector.
@@ -147,6 +165,7 @@ __device__ __forceinline__ uint32_t store4(void* C, int64_t ldc, int64_t m, int6
 
 // ------------------------------------------------------------ main kernel
 constexpr int kBM = 256, kBN = 256, kBK = 128, kThreads = 256;
+constexpr int kMainThreads = 512;      // 8 waves: two groups of four
 constexpr int kTileBytes = kBM * kBK;  // one operand tile, 32 KiB
 
 // Direct L2 -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4, the
@@ -179,8 +198,14 @@ __device__ __forceinline__ void st_stream(void* p, uint4 v) {
     __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w}, (u32x4*)p);
 }
 
-// Epilogue staging rows (bytes): 32 output rows of a wave per pass.
+// Epilogue staging rows (bytes): 32 output rows of a wave per pass; the
+// codes of the fused quantise (256 x 256 bytes) follow the bf16 staging area.
 constexpr int kEpRowBf16 = 128 * 2 + 16, kEpRowF32 = 128 * 4 + 16;
+constexpr int kEpBf16Bytes = 8 * 32 * kEpRowBf16, kEpF32Bytes = 8 * 32 * kEpRowF32;
+constexpr int kCodesOff = kEpBf16Bytes;
+constexpr int kSmemBytes = kCodesOff + kBM * kBN > kEpF32Bytes ? kCodesOff + kBM * kBN : kEpF32Bytes;
+static_assert(kSmemBytes >= 2 * 2 * kTileBytes && kSmemBytes <= 160 * 1024, "LDS budget");
+static_assert(kCodesOff % 16 == 0, "codes staging alignment");
 
 // Output codes of the fused quantise (QF >= 0, bf16 output only): Y8 [M, N]
 // and optionally Y8T [N, M] in format QF, cast with a predicted bias; the
@@ -198,21 +223,23 @@ struct QuantOut {
 };
 
 template <int FA, int FB, int OUT_DT, bool AMAX, int QF = -1>
-__global__ __launch_bounds__(kThreads) void gemm_nt_256(
+__global__ __launch_bounds__(kMainThreads) void gemm_nt_256(
     const uint8_t* __restrict__ A, const uint8_t* __restrict__ B, const int32_t* __restrict__ ba_p,
     const int32_t* __restrict__ bb_p, void* __restrict__ C, int M, int N, int K, int tiles_m,
     int tiles_n, int vec_out, uint32_t* __restrict__ amax_out, QuantOut qo) {
     static_assert(QF < 0 || OUT_DT == FP8_DT_BF16, "fused quantise is for bf16 outputs");
-    __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * 2 * kTileBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[kSmemBytes];
 
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    // group (0: waves 0-3, 1: waves 4-7) and quadrant; wave-uniform
+    const int g = __builtin_amdgcn_readfirstlane(w >> 2), sq = __builtin_amdgcn_readfirstlane(w & 3);
     int tm, tn;
     tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
     const int m0 = tm * kBM, n0 = tn * kBN;
 
-    // Loader: wave w fills rows [64 w, 64 w + 64) of both tiles, 8 rows per
-    // copy (voff[0..7] for A, voff[8..15] for B); lane -> row r =
-    // 64 w + 8 i + lane / 8 and physical chunk lane % 8, which holds logical
+    // Loader (group 0): wave sq fills rows [64 sq, 64 sq + 64) of both tiles,
+    // 8 rows per copy (voff[0..7] for A, voff[8..15] for B); lane -> row r =
+    // 64 sq + 8 i + lane / 8 and physical chunk lane % 8, which holds logical
     // chunk (lane % 8) ^ chunk_swz(r).  Rows past the matrix edge re-read the
     // last row (their outputs are not stored).  Offsets are relative to the
     // tile's first row, so they fit 32 bits for K < 2^22.
@@ -220,7 +247,7 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_256(
     uint32_t voff[16];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-        const int r = w * 64 + i * 8 + lrow;
+        const int r = sq * 64 + i * 8 + lrow;
         const int lchunk = (lane & 7) ^ chunk_swz(r);
         voff[i] = (uint32_t)((min(m0 + r, M - 1) - m0) * K + lchunk * 16);
         voff[8 + i] = (uint32_t)((min(n0 + r, N - 1) - n0) * K + lchunk * 16);
@@ -229,61 +256,88 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_256(
     const uint8_t* baseB = B + (int64_t)n0 * K;
     // LDS address of this wave's first loader row (wave-uniform); copy d of
     // 16 goes to operand d / 8, row group d % 8.
-    const uint32_t lds_w = __builtin_amdgcn_readfirstlane(lds_addr(smem) + w * 64 * kBK);
+    const uint32_t lds_w = __builtin_amdgcn_readfirstlane(lds_addr(smem) + sq * 64 * kBK);
     auto dma = [&](int d, int stage, int k0) {
         lds_dma16_s((d >= 8 ? baseB : baseA) + k0, voff[d],
                     lds_w + stage * 2 * kTileBytes + (d >= 8 ? kTileBytes : 0) + (d & 7) * 8 * kBK);
     };
 
-    const int wm = w >> 1, wn = w & 1;
+    // this wave's sub-tile: rows [wr0, wr0 + 64), columns [wc0, wc0 + 128) of the tile
+    const int wr0 = (sq >> 1) * 128 + g * 64, wc0 = (sq & 1) * 128;
     const int frow = lane & 15, fg = lane >> 4;
     // byte offsets (within a 16-row block) of this lane's two fragment pieces
     const int fo0 = frow * kBK + (((2 * fg) ^ chunk_swz(frow)) << 4);
     const int fo1 = frow * kBK + (((2 * fg + 1) ^ chunk_swz(frow)) << 4);
 
-    v4f acc[8][8];
+    v4f acc[4][8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 8; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
-    // Software pipeline, one barrier per k-step.  At the top of step kt every
-    // wave waits for its own copies of tile kt, then the barrier makes all of
-    // them visible and also guarantees that every wave has finished reading
-    // the other buffer (step kt-1), which the copies of tile kt+1 overwrite.
-    // Those 16 copies are issued one per two MFMAs over the first 32 (the
-    // vector-memory path of a CU takes about 1 KiB per 16 cycles, so a copy
-    // per MFMA from all four waves would stall issue); B fragments are read
-    // 4 MFMAs ahead of use, the next A fragment two MFMAs into the current row.
+    // Ping-pong pipeline.  Phases are separated by workgroup barriers; in
+    // every phase one group issues MFMAs and the other loads:
+    //   phase 1:        group 0 loads fragments of step 0
+    //   phase 2k + 2:   group 0 MFMAs of step k,   group 1 loads step k
+    //   phase 2k + 3:   group 0 loads step k + 1,  group 1 MFMAs of step k
+    // A load phase reads all 24 fragment pieces of the wave's next step and
+    // waits for them before the barrier.  Tile k sits in buffer k % 2; group 0
+    // copies tile k + 1 into the other buffer in its load phase of step k
+    // (tiles 0 and 1 before phase 1), after both groups have read tile k - 1
+    // from it, and waits for those copies at the end of its next MFMA phase,
+    // before either group reads tile k + 1.  Every wave passes 2 nk + 1
+    // barriers (group 1 passes one before its first load phase and none after
+    // its last MFMA phase), so the groups stay in step.
     const int nk = K / kBK;
-    if (nk > 0) {
+    if (g == 0 && nk > 0) {
 #pragma unroll
         for (int d = 0; d < 16; ++d) dma(d, 0, 0);
+        if (nk > 1) {
+#pragma unroll
+            for (int d = 0; d < 16; ++d) dma(d, 1, kBK);
+            wait_vmcnt<16>();
+        } else {
+            wait_vmcnt<0>();
+        }
     }
+    if (nk > 0) {
+        ws_barrier();
+        if (g == 1) ws_barrier();
+    }
+    v8i af[4], bf[8];
     for (int kt = 0; kt < nk; ++kt) {
-        const int st = kt & 1;
-        const bool more = kt + 1 < nk;
-        const int k1 = (kt + 1) * kBK;
-        wait_vmcnt<0>();
-        __syncthreads();
-        const uint8_t* sa = smem + st * 2 * kTileBytes + wm * 128 * kBK;
-        const uint8_t* sb = smem + st * 2 * kTileBytes + kTileBytes + wn * 128 * kBK;
-        v8i bf[8], af[2];
-        af[0] = ld_frag(sa, fo0, fo1);
+        const uint8_t* sa = smem + (kt & 1) * 2 * kTileBytes + wr0 * kBK;
+        const uint8_t* sb = smem + (kt & 1) * 2 * kTileBytes + kTileBytes + wc0 * kBK;
+        if (g == 0 && kt >= 1 && kt + 1 < nk) {
+            const int st = (kt + 1) & 1, k1 = (kt + 1) * kBK;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) bf[j] = ld_frag(sb + j * 16 * kBK, fo0, fo1);
-        __builtin_amdgcn_sched_barrier(0);
+            for (int q = 0; q < 12; ++q) {
+                if (q < 4) af[q] = ld_frag(sa + q * 16 * kBK, fo0, fo1);
+                else bf[q - 4] = ld_frag(sb + (q - 4) * 16 * kBK, fo0, fo1);
+                dma(q, st, k1);
+                if (q < 4) dma(12 + q, st, k1);
+            }
+        } else {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
+            for (int q = 0; q < 12; ++q) {
+                if (q < 4) af[q] = ld_frag(sa + q * 16 * kBK, fo0, fo1);
+                else bf[q - 4] = ld_frag(sb + (q - 4) * 16 * kBK, fo0, fo1);
+            }
+        }
+        wait_lgkmcnt0();
+        ws_barrier();
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
-                const int q = i * 8 + j;
-                if (i == 0 && j + 4 < 8) bf[j + 4] = ld_frag(sb + (j + 4) * 16 * kBK, fo0, fo1);
-                if (j == 2 && i + 1 < 8) af[(i + 1) & 1] = ld_frag(sa + (i + 1) * 16 * kBK, fo0, fo1);
-                if (more && (q & 1) == 0 && q < 32) dma(q >> 1, st ^ 1, k1);
-                acc[i][j] = mfma16<FB, FA>(bf[j], af[i & 1], acc[i][j]);
+                acc[i][j] = mfma16<FB, FA>(bf[j], af[i], acc[i][j]);
                 __builtin_amdgcn_sched_barrier(0);
             }
+        if (g == 0) {
+            wait_vmcnt<0>();
+            ws_barrier();
+        } else if (kt + 1 < nk) {
+            ws_barrier();
         }
     }
 
@@ -292,22 +346,24 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_256(
     // store writes 16-byte pieces of whole 256-byte (bf16) or 512-byte (fp32)
     // row runs.  Staging reads map one LDS read phase (lane bit 5 and the
     // parity of lane bits 2..4) to one row, so they are free of bank conflicts.
+    // The last barrier of the main loop follows every read of the operand
+    // tiles, so group 0 stages and stores its outputs while group 1 issues its
+    // last MFMAs.
     const int sh = -(*ba_p + *bb_p);
-    __syncthreads();  // every wave is done with the operand tiles
     const int prow = 2 * (lane >> 5) + (((lane >> 2) ^ (lane >> 3) ^ (lane >> 4)) & 1);
     uint32_t mx = 0;
     if (OUT_DT == FP8_DT_BF16) {
         uint8_t* ep = smem + w * 32 * kEpRowBf16;
         typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
         u16x2 m2 = {0, 0};
-        // Fused quantise: the codes of the tile, row-major, in the upper 64 KiB
-        // (row r = 256 bytes; 16-byte chunk c stored at chunk c ^ (r % 16)).
-        uint8_t* cs = smem + 2 * kTileBytes;
+        // Fused quantise: the codes of the tile, row-major, after the staging
+        // rows (row r = 256 bytes; 16-byte chunk c stored at chunk c ^ (r % 16)).
+        uint8_t* cs = smem + kCodesOff;
         int bq = 0;
-        uint32_t codes[8][8];
+        uint32_t codes[4][8];
         if (QF >= 0) bq = clamp_bias(*qo.pred);
 #pragma unroll
-        for (int i2 = 0; i2 < 4; ++i2) {
+        for (int i2 = 0; i2 < 2; ++i2) {
 #pragma unroll
             for (int ii = 0; ii < 2; ++ii) {
                 const int i = 2 * i2 + ii;
@@ -326,7 +382,7 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_256(
                             c4 = nan_patch<QF < 0 ? 0 : QF>(c4, hs);
                         }
                         codes[i][j] = c4;
-                        const int r = wm * 128 + i * 16 + frow, col = wn * 128 + j * 16 + 4 * fg;
+                        const int r = wr0 + i * 16 + frow, col = wc0 + j * 16 + 4 * fg;
                         *(uint32_t*)(cs + r * 256 + ((((col >> 4) ^ r) & 15) << 4) + (col & 15)) = c4;
                     }
                     *(uint2*)(ep + (ii * 16 + frow) * kEpRowBf16 + (j * 16 + 4 * fg) * 2) = make_uint2(lo, hi);
@@ -336,7 +392,7 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_256(
             for (int t = 0; t < 8; ++t) {
                 const int row = 4 * t + prow, c16 = lane & 15;
                 const uint4 v = *(const uint4*)(ep + row * kEpRowBf16 + c16 * 16);
-                const int64_t m = m0 + wm * 128 + i2 * 32 + row, n = n0 + wn * 128 + c16 * 8;
+                const int64_t m = m0 + wr0 + i2 * 32 + row, n = n0 + wc0 + c16 * 8;
                 if (m < M) {
                     uint16_t* p = (uint16_t*)C + m * N + n;
                     if (vec_out && n + 8 <= N) {
@@ -350,11 +406,11 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_256(
         }
         mx = (uint32_t)max(m2.x, m2.y) << 16;
         if (QF >= 0) {
-            // Y8 rows from the staged codes: 4096 chunks of 16 bytes, 16 per thread.
+            // Y8 rows from the staged codes: 4096 chunks of 16 bytes, 8 per thread.
             __syncthreads();
 #pragma unroll
-            for (int h = 0; h < 16; ++h) {
-                const int idx = threadIdx.x + h * kThreads, r = idx >> 4, c = idx & 15;
+            for (int h = 0; h < 8; ++h) {
+                const int idx = threadIdx.x + h * kMainThreads, r = idx >> 4, c = idx & 15;
                 const uint4 v = *(const uint4*)(cs + r * 256 + (((c ^ r) & 15) << 4));
                 const int64_t m = m0 + r, n = n0 + c * 16;
                 if (m < M && n < N) {
@@ -372,10 +428,10 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_256(
                 // rows; chunk q of column c stored at chunk q ^ (c % 16)).
                 __syncthreads();
 #pragma unroll
-                for (int i = 0; i < 8; ++i)
+                for (int i = 0; i < 4; ++i)
 #pragma unroll
                     for (int j = 0; j < 8; ++j) {
-                        const int r = wm * 128 + i * 16 + frow, col0 = wn * 128 + j * 16 + 4 * fg;
+                        const int r = wr0 + i * 16 + frow, col0 = wc0 + j * 16 + 4 * fg;
 #pragma unroll
                         for (int e = 0; e < 4; ++e) {
                             const int c = col0 + e;
@@ -384,8 +440,8 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_256(
                     }
                 __syncthreads();
 #pragma unroll
-                for (int h = 0; h < 16; ++h) {
-                    const int idx = threadIdx.x + h * kThreads, c = idx >> 4, q = idx & 15;
+                for (int h = 0; h < 8; ++h) {
+                    const int idx = threadIdx.x + h * kMainThreads, c = idx >> 4, q = idx & 15;
                     const uint4 v = *(const uint4*)(cs + c * 256 + (((q ^ c) & 15) << 4));
                     const int64_t n = n0 + c, m = m0 + q * 16;
                     if (n < N && m < M) {
@@ -403,7 +459,7 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_256(
     } else {
         uint8_t* ep = smem + w * 32 * kEpRowF32;
 #pragma unroll
-        for (int i2 = 0; i2 < 4; ++i2) {
+        for (int i2 = 0; i2 < 2; ++i2) {
 #pragma unroll
             for (int ii = 0; ii < 2; ++ii) {
                 const int i = 2 * i2 + ii;
@@ -423,7 +479,7 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_256(
             for (int t = 0; t < 16; ++t) {
                 const int row = 2 * t + (lane >> 5), c32 = lane & 31;
                 const float4 v = *(const float4*)(ep + row * kEpRowF32 + c32 * 16);
-                const int64_t m = m0 + wm * 128 + i2 * 32 + row, n = n0 + wn * 128 + c32 * 4;
+                const int64_t m = m0 + wr0 + i2 * 32 + row, n = n0 + wc0 + c32 * 4;
                 if (m < M) {
                     float* p = (float*)C + m * N + n;
                     if (vec_out && n + 4 <= N) {
@@ -436,20 +492,25 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_256(
             }
         }
     }
-    if (AMAX) {
-        // rows and columns past the edge computed clamped copies of real ones,
-        // so including them cannot change the maximum
-        mx = wave_max_u32(mx);
-        if (lane == 0) atomicMax(amax_out, mx);
-    }
-    if (QF >= 0) {  // this workgroup's largest |Y| (bf16 magnitude pattern)
-        __shared__ uint32_t wmx[kThreads / 64];
-        const uint32_t m16 = wave_max_u32(mx >> 16);
-        if (lane == 0) wmx[w] = m16;
+    if (AMAX || QF >= 0) {
+        // The workgroup's largest |Y| pattern: one global atomic per workgroup
+        // (the waves of all resident workgroups finish together, and atomics
+        // on one word from every wave would queue behind each other).  Rows
+        // and columns past the edge computed clamped copies of real ones, so
+        // including them cannot change the maximum.
+        __shared__ uint32_t wmx[kMainThreads / 64];
+        const uint32_t wv = wave_max_u32(mx);
+        if (lane == 0) wmx[w] = wv;
         __syncthreads();
         if (threadIdx.x == 0) {
-            qo.parts[blockIdx.x] = max(max(wmx[0], wmx[1]), max(wmx[2], wmx[3]));
-            if (blockIdx.x == 0) *qo.used = bq_used(qo.pred);
+            uint32_t b = 0;
+#pragma unroll
+            for (int v = 0; v < kMainThreads / 64; ++v) b = max(b, wmx[v]);
+            if (AMAX) atomicMax(amax_out, b);
+            if (QF >= 0) {  // bf16 magnitude pattern
+                qo.parts[blockIdx.x] = b >> 16;
+                if (blockIdx.x == 0) *qo.used = bq_used(qo.pred);
+            }
         }
     }
 }
@@ -657,7 +718,7 @@ void launch_t(const uint8_t* A, const int32_t* ba, const uint8_t* B, const int32
     } else if (fast) {
         const int tiles_m = (int)((M + kBM - 1) / kBM), tiles_n = (int)((N + kBN - 1) / kBN);
         const int vec16 = ((uintptr_t)C % 16 == 0) && ((N * esz) % 16 == 0);
-        hipLaunchKernelGGL((gemm_nt_256<FA, FB, OUT_DT, AMAX>), dim3(tiles_m * tiles_n), dim3(kThreads), 0,
+        hipLaunchKernelGGL((gemm_nt_256<FA, FB, OUT_DT, AMAX>), dim3(tiles_m * tiles_n), dim3(kMainThreads), 0,
                            s, A, B, ba, bb, C, (int)M, (int)N, (int)K, tiles_m, tiles_n, vec16, amax, QuantOut{});
     } else {
         const int64_t tiles_m = (M + kSBM - 1) / kSBM, tiles_n = (N + kSBN - 1) / kSBN;
@@ -683,7 +744,7 @@ void launch_fused_t(const uint8_t* A, const int32_t* ba, const uint8_t* B, const
                     int64_t M, int64_t N, int64_t K, const QuantOut& qo, hipStream_t s) {
     const int tiles_m = (int)((M + kBM - 1) / kBM), tiles_n = (int)((N + kBN - 1) / kBN);
     const int vec16 = ((uintptr_t)C % 16 == 0) && ((N * 2) % 16 == 0);
-    hipLaunchKernelGGL((gemm_nt_256<FA, FB, FP8_DT_BF16, false, QF>), dim3(tiles_m * tiles_n), dim3(kThreads), 0,
+    hipLaunchKernelGGL((gemm_nt_256<FA, FB, FP8_DT_BF16, false, QF>), dim3(tiles_m * tiles_n), dim3(kMainThreads), 0,
                        s, A, B, ba, bb, C, (int)M, (int)N, (int)K, tiles_m, tiles_n, vec16, nullptr, qo);
 }
 
