@@ -52,6 +52,9 @@ def parse():
                         "fp8_quantise without prediction, fp8_scale_bias + fp8_cast, or FP8-CSCALE "
                         "(constant bias --cscale-bias, no amax: not the headline metric)")
     p.add_argument("--cscale-bias", type=int, default=0)
+    p.add_argument("--bias", choices=("fused", "separate"), default="fused",
+                   help="bias of Y and dX: taken by the matmul launch itself (last workgroup), "
+                        "or epilogue amax + fp8_bias_from_amax (identical bits)")
     p.add_argument("--launch", choices=("graph", "eager"), default="graph",
                    help="timed steps: replays of one HIP graph holding the whole step, or "
                         "one host call per library call")
@@ -273,7 +276,7 @@ def main():
     tens = {k: v.to(dev) for k, v in cpu.items()}
     torch.cuda.synchronize()
     step = L.WorkloadStep(w, tens, dev, margin=args.margin, quant=args.quant,
-                          cscale_bias=args.cscale_bias)
+                          cscale_bias=args.cscale_bias, fused_bias=args.bias == "fused")
     if not w.train:
         step.prepare_inference()
     flush = None
@@ -305,6 +308,7 @@ def main():
                    "mode": "train fwd+bwd" if w.train else "PTQ inference fwd",
                    "accumulate": "fp32", "outputs": "Y,dX bf16; dW fp32",
                    "margin": args.margin, "mall_flush_mb": args.flush_mb, "quant": args.quant,
+                   "output_bias": args.bias,
                    "launch": "one HIP graph replay per step" if args.launch == "graph"
                    else "one host call per library call"},
         "frac_of_fp8_peak": round(value / FP8_PEAK_TFLOPS, 4),

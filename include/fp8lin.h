@@ -211,6 +211,32 @@ int32_t fp8_linear_bwd_dx(const uint8_t *dy8, const int32_t *bg, const uint8_t *
                           int64_t K, uint32_t *dx_amax_bits, void *stream);
 
 /*
+ * fp8_linear_fwd_bias / fp8_linear_bwd_dx_bias -- fp8_linear_fwd /
+ * fp8_linear_bwd_dx with the amax of the output turned into the Eq. 3 bias
+ * (Sec. 3) for the layer that consumes it, in the same launch: the same
+ * y / dx, bias, amax and flags as the matmul with y_amax_bits followed by
+ * fp8_bias_from_amax, without the separate zeroing and bias launches (the
+ * last workgroup of the matmul to finish computes the bias).
+ * y / dx:  out, as fp8_linear_fwd / fp8_linear_bwd_dx (bf16 or fp32).
+ * *_fmt, margin: format and margin of the bias (as fp8_scale_bias).
+ * *_bias:  out, the bias.  *_amax_bits, *_flags: out, optional (NULL).
+ * ws:      workspace of fp8_linear_bias_ws_bytes() bytes, 4-byte aligned,
+ *          which must hold zeros before the first call; every call that
+ *          returns FP8_OK and runs to completion leaves it zero again.
+ *          Calls that may run at the same time need separate workspaces.
+ * M == 0 or N == 0 (no output): bias 0, amax 0, flags FP8_FLAG_ZERO.
+ */
+size_t fp8_linear_bias_ws_bytes(void);
+int32_t fp8_linear_fwd_bias(const uint8_t *x8, const int32_t *bx, const uint8_t *w8t, const int32_t *bw,
+                            void *y, int32_t y_dt, int64_t M, int64_t N, int64_t K, int32_t y_fmt,
+                            int32_t margin, int32_t *y_bias, uint32_t *y_amax_bits, uint32_t *y_flags,
+                            void *ws, size_t ws_bytes, void *stream);
+int32_t fp8_linear_bwd_dx_bias(const uint8_t *dy8, const int32_t *bg, const uint8_t *w8, const int32_t *bw,
+                               void *dx, int32_t dx_dt, int64_t M, int64_t N, int64_t K, int32_t dx_fmt,
+                               int32_t margin, int32_t *dx_bias, uint32_t *dx_amax_bits, uint32_t *dx_flags,
+                               void *ws, size_t ws_bytes, void *stream);
+
+/*
  * fp8_linear_fwd_quantise / fp8_linear_bwd_dx_quantise -- the matmul of
  * fp8_linear_fwd / fp8_linear_bwd_dx (bf16 output) with the amax, Eq. 3 bias
  * and cast of its output fused into the epilogue, for the next layer that

@@ -148,6 +148,50 @@ int32_t fp8_linear_bwd_dw(const uint8_t* x8t, const int32_t* bx, const uint8_t* 
     return gemm_common(x8t, FP8_E4M3, bx, dy8t, FP8_E5M2, bg, dw, dw_dt, K, N, M, nullptr, stream);
 }
 
+size_t fp8_linear_bias_ws_bytes(void) { return 2 * sizeof(uint32_t); }
+
+namespace {
+// C [rows, cols] = 2^-(*ba + *bb) A [rows, kc] . B [cols, kc]^T with the Eq. 3
+// bias of C taken in the same launch (see fp8_linear_fwd_bias).
+int32_t gemm_bias_common(const uint8_t* a, int fa, const int32_t* ba, const uint8_t* b, int fb,
+                         const int32_t* bb, void* c, int32_t c_dt, int64_t rows, int64_t cols, int64_t kc,
+                         int32_t fmt, int32_t margin, int32_t* bias, uint32_t* amax_bits, uint32_t* flags,
+                         void* ws, size_t ws_bytes, void* stream) {
+    if (!dt_ok(c_dt) || !fmt_ok(fmt) || rows < 0 || cols < 0 || kc < 0 || rows > kMaxDim || cols > kMaxDim ||
+        kc > kMaxDim)
+        return FP8_EINVAL;
+    if (margin < -FP8_MAX_MARGIN || margin > FP8_MAX_MARGIN) return FP8_EINVAL;
+    if (!bias || !aligned(bias, 4)) return FP8_EINVAL;
+    if ((amax_bits && !aligned(amax_bits, 4)) || (flags && !aligned(flags, 4))) return FP8_EINVAL;
+    if (!ws || !aligned(ws, 4) || ws_bytes < fp8_linear_bias_ws_bytes()) return FP8_EINVAL;
+    if (rows == 0 || cols == 0)  // an empty output has amax 0
+        return launch_scale_bias(nullptr, FP8_DT_BF16, 0, fmt, margin, bias, amax_bits, flags, nullptr,
+                                 as_stream(stream));
+    if (!c || !ba || !bb || (kc > 0 && (!a || !b))) return FP8_EINVAL;
+    if (!aligned(c, esize(c_dt)) || !aligned(ba, 4) || !aligned(bb, 4)) return FP8_EINVAL;
+    if (rows > INT32_MAX || cols > INT32_MAX) return FP8_ENOTSUP;
+    return launch_gemm_nt_bias(a, fa, ba, b, fb, bb, c, c_dt, rows, cols, kc, fmt, margin, bias, amax_bits, flags,
+                               (uint32_t*)ws, as_stream(stream));
+}
+}  // namespace
+
+int32_t fp8_linear_fwd_bias(const uint8_t* x8, const int32_t* bx, const uint8_t* w8t, const int32_t* bw,
+                            void* y, int32_t y_dt, int64_t M, int64_t N, int64_t K, int32_t y_fmt,
+                            int32_t margin, int32_t* y_bias, uint32_t* y_amax_bits, uint32_t* y_flags,
+                            void* ws, size_t ws_bytes, void* stream) {
+    return gemm_bias_common(x8, FP8_E4M3, bx, w8t, FP8_E4M3, bw, y, y_dt, M, N, K, y_fmt, margin, y_bias,
+                            y_amax_bits, y_flags, ws, ws_bytes, stream);
+}
+
+int32_t fp8_linear_bwd_dx_bias(const uint8_t* dy8, const int32_t* bg, const uint8_t* w8, const int32_t* bw,
+                               void* dx, int32_t dx_dt, int64_t M, int64_t N, int64_t K, int32_t dx_fmt,
+                               int32_t margin, int32_t* dx_bias, uint32_t* dx_amax_bits, uint32_t* dx_flags,
+                               void* ws, size_t ws_bytes, void* stream) {
+    // dX [M, K] = dY8 [M, N] . W8 [K, N]^T: contraction over N.
+    return gemm_bias_common(dy8, FP8_E5M2, bg, w8, FP8_E4M3, bw, dx, dx_dt, M, K, N, dx_fmt, margin, dx_bias,
+                            dx_amax_bits, dx_flags, ws, ws_bytes, stream);
+}
+
 size_t fp8_linear_quantise_ws_bytes(int64_t M, int64_t N) {
     if (M <= 0 || N <= 0 || M > kMaxDim || N > kMaxDim) return 0;
     return (size_t)gemm_quantise_ws_words(M, N) * sizeof(uint32_t);

@@ -222,11 +222,32 @@ struct QuantOut {
     int vec8, vec8t;  // 16-byte stores allowed
 };
 
+// Eq. 3 bias of the output taken in the same launch (ws != nullptr): every
+// workgroup folds its largest |Y| pattern into ws[0] and then counts itself
+// in ws[1]; the last one to count takes the total, writes amax, bias and
+// flags, and leaves both words zero for the next call.
+struct BiasOut {
+    int32_t* bias;
+    uint32_t* flags;  // may be null
+    uint32_t* ws;     // [0] running maximum, [1] finished workgroups; zero between calls
+    int fmt;
+    int32_t margin;
+};
+
+__device__ __forceinline__ int32_t bias_of_fmt(int fmt, uint32_t a, int32_t margin, uint32_t* fl) {
+    switch (fmt) {
+        case FP8_E4M3: return bias_of<FP8_E4M3>(a, margin, fl);
+        case FP8_E5M2: return bias_of<FP8_E5M2>(a, margin, fl);
+        case FP8_E4_A: return bias_of<FP8_E4_A>(a, margin, fl);
+        default: return bias_of<FP8_E5_A>(a, margin, fl);
+    }
+}
+
 template <int FA, int FB, int OUT_DT, bool AMAX, int QF = -1>
 __global__ __launch_bounds__(kMainThreads) void gemm_nt_256(
     const uint8_t* __restrict__ A, const uint8_t* __restrict__ B, const int32_t* __restrict__ ba_p,
     const int32_t* __restrict__ bb_p, void* __restrict__ C, int M, int N, int K, int tiles_m,
-    int tiles_n, int vec_out, uint32_t* __restrict__ amax_out, QuantOut qo) {
+    int tiles_n, int vec_out, uint32_t* __restrict__ amax_out, QuantOut qo, BiasOut bo) {
     static_assert(QF < 0 || OUT_DT == FP8_DT_BF16, "fused quantise is for bf16 outputs");
     __shared__ __attribute__((aligned(1024))) uint8_t smem[kSmemBytes];
 
@@ -506,7 +527,23 @@ __global__ __launch_bounds__(kMainThreads) void gemm_nt_256(
             uint32_t b = 0;
 #pragma unroll
             for (int v = 0; v < kMainThreads / 64; ++v) b = max(b, wmx[v]);
-            if (AMAX) atomicMax(amax_out, b);
+            if (AMAX && !bo.ws) atomicMax(amax_out, b);
+            if (AMAX && bo.ws) {
+                // The fold returns its old value, which is consumed before the
+                // count is issued, so the fold has been performed by then; the
+                // workgroup that counts last therefore sees every fold.
+                const uint32_t prev = __hip_atomic_fetch_max(bo.ws, b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                asm volatile("; fold returned %0" : : "v"(prev));
+                const uint32_t done = __hip_atomic_fetch_add(bo.ws + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (done == gridDim.x - 1) {
+                    const uint32_t a = __hip_atomic_exchange(bo.ws, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(bo.ws + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    uint32_t fl;
+                    *bo.bias = bias_of_fmt(bo.fmt, a, bo.margin, &fl);
+                    if (amax_out) *amax_out = a;
+                    if (bo.flags) *bo.flags = fl;
+                }
+            }
             if (QF >= 0) {  // bf16 magnitude pattern
                 qo.parts[blockIdx.x] = b >> 16;
                 if (blockIdx.x == 0) *qo.used = bq_used(qo.pred);
@@ -705,13 +742,20 @@ __global__ void fill_u32_kernel(uint32_t* p, uint32_t v) {
     if (threadIdx.x == 0 && blockIdx.x == 0) *p = v;
 }
 
+// The LDS-staged kernels need K a multiple of 128, 16-byte aligned operands
+// and 32-bit offsets within a tile.
+bool fast_path(const uint8_t* A, const uint8_t* B, int64_t M, int64_t N, int64_t K) {
+    return (K % kBK == 0) && ((uintptr_t)A % 16 == 0) && ((uintptr_t)B % 16 == 0) && M <= INT32_MAX &&
+           N <= INT32_MAX && K < (1 << 22);
+}
+
+// bo.ws != nullptr only where the 256 x 256 kernel runs (fast_path, M > 32).
 template <int FA, int FB, int OUT_DT, bool AMAX>
 void launch_t(const uint8_t* A, const int32_t* ba, const uint8_t* B, const int32_t* bb, void* C,
-              int64_t M, int64_t N, int64_t K, uint32_t* amax, hipStream_t s) {
+              int64_t M, int64_t N, int64_t K, uint32_t* amax, const BiasOut& bo, hipStream_t s) {
     const int esz = OUT_DT == FP8_DT_BF16 ? 2 : 4;
     const int vec_out = ((uintptr_t)C % (4 * esz) == 0) && (N % 4 == 0);
-    const bool fast = (K % kBK == 0) && ((uintptr_t)A % 16 == 0) && ((uintptr_t)B % 16 == 0) &&
-                      M <= INT32_MAX && N <= INT32_MAX && K < (1 << 22);
+    const bool fast = fast_path(A, B, M, N, K);
     if (fast && M <= 32) {
         if (M <= 16) launch_decode<FA, FB, OUT_DT, AMAX, 1>(A, ba, B, bb, C, (int)M, (int)N, (int)K, vec_out, amax, s);
         else launch_decode<FA, FB, OUT_DT, AMAX, 2>(A, ba, B, bb, C, (int)M, (int)N, (int)K, vec_out, amax, s);
@@ -719,7 +763,7 @@ void launch_t(const uint8_t* A, const int32_t* ba, const uint8_t* B, const int32
         const int tiles_m = (int)((M + kBM - 1) / kBM), tiles_n = (int)((N + kBN - 1) / kBN);
         const int vec16 = ((uintptr_t)C % 16 == 0) && ((N * esz) % 16 == 0);
         hipLaunchKernelGGL((gemm_nt_256<FA, FB, OUT_DT, AMAX>), dim3(tiles_m * tiles_n), dim3(kMainThreads), 0,
-                           s, A, B, ba, bb, C, (int)M, (int)N, (int)K, tiles_m, tiles_n, vec16, amax, QuantOut{});
+                           s, A, B, ba, bb, C, (int)M, (int)N, (int)K, tiles_m, tiles_n, vec16, amax, QuantOut{}, bo);
     } else {
         const int64_t tiles_m = (M + kSBM - 1) / kSBM, tiles_n = (N + kSBN - 1) / kSBN;
         hipLaunchKernelGGL((gemm_nt_small<FA, FB, OUT_DT, AMAX>), dim3((unsigned)(tiles_m * tiles_n)),
@@ -727,16 +771,31 @@ void launch_t(const uint8_t* A, const int32_t* ba, const uint8_t* B, const int32
     }
 }
 
+// with_amax: epilogue amax (into *amax, or folded into bo.ws).
 template <int FA, int FB>
 void dispatch_out(const uint8_t* A, const int32_t* ba, const uint8_t* B, const int32_t* bb, void* C,
-                  int out_dt, int64_t M, int64_t N, int64_t K, uint32_t* amax, hipStream_t s) {
+                  int out_dt, int64_t M, int64_t N, int64_t K, bool with_amax, uint32_t* amax,
+                  const BiasOut& bo, hipStream_t s) {
     if (out_dt == FP8_DT_BF16) {
-        if (amax) launch_t<FA, FB, FP8_DT_BF16, true>(A, ba, B, bb, C, M, N, K, amax, s);
-        else launch_t<FA, FB, FP8_DT_BF16, false>(A, ba, B, bb, C, M, N, K, amax, s);
+        if (with_amax) launch_t<FA, FB, FP8_DT_BF16, true>(A, ba, B, bb, C, M, N, K, amax, bo, s);
+        else launch_t<FA, FB, FP8_DT_BF16, false>(A, ba, B, bb, C, M, N, K, amax, bo, s);
     } else {
-        if (amax) launch_t<FA, FB, FP8_DT_F32, true>(A, ba, B, bb, C, M, N, K, amax, s);
-        else launch_t<FA, FB, FP8_DT_F32, false>(A, ba, B, bb, C, M, N, K, amax, s);
+        if (with_amax) launch_t<FA, FB, FP8_DT_F32, true>(A, ba, B, bb, C, M, N, K, amax, bo, s);
+        else launch_t<FA, FB, FP8_DT_F32, false>(A, ba, B, bb, C, M, N, K, amax, bo, s);
     }
+}
+
+void dispatch_fmts(const uint8_t* A, int fa, const int32_t* ba, const uint8_t* B, int fb, const int32_t* bb,
+                   void* C, int out_dt, int64_t M, int64_t N, int64_t K, bool with_amax, uint32_t* amax,
+                   const BiasOut& bo, hipStream_t s) {
+    if (fa == FP8_E4M3 && fb == FP8_E4M3)
+        dispatch_out<FP8_E4M3, FP8_E4M3>(A, ba, B, bb, C, out_dt, M, N, K, with_amax, amax, bo, s);
+    else if (fa == FP8_E5M2 && fb == FP8_E4M3)
+        dispatch_out<FP8_E5M2, FP8_E4M3>(A, ba, B, bb, C, out_dt, M, N, K, with_amax, amax, bo, s);
+    else if (fa == FP8_E4M3 && fb == FP8_E5M2)
+        dispatch_out<FP8_E4M3, FP8_E5M2>(A, ba, B, bb, C, out_dt, M, N, K, with_amax, amax, bo, s);
+    else
+        dispatch_out<FP8_E5M2, FP8_E5M2>(A, ba, B, bb, C, out_dt, M, N, K, with_amax, amax, bo, s);
 }
 
 template <int FA, int FB, int QF>
@@ -745,7 +804,7 @@ void launch_fused_t(const uint8_t* A, const int32_t* ba, const uint8_t* B, const
     const int tiles_m = (int)((M + kBM - 1) / kBM), tiles_n = (int)((N + kBN - 1) / kBN);
     const int vec16 = ((uintptr_t)C % 16 == 0) && ((N * 2) % 16 == 0);
     hipLaunchKernelGGL((gemm_nt_256<FA, FB, FP8_DT_BF16, false, QF>), dim3(tiles_m * tiles_n), dim3(kMainThreads), 0,
-                       s, A, B, ba, bb, C, (int)M, (int)N, (int)K, tiles_m, tiles_n, vec16, nullptr, qo);
+                       s, A, B, ba, bb, C, (int)M, (int)N, (int)K, tiles_m, tiles_n, vec16, nullptr, qo, BiasOut{});
 }
 
 template <int FA, int FB>
@@ -772,8 +831,7 @@ int32_t launch_gemm_nt_quantise(const uint8_t* A, int fa, const int32_t* ba, con
                                 int32_t margin, const int32_t* pred, int32_t* bias, uint32_t* amax_bits,
                                 uint32_t* flags, uint8_t* y8, int64_t ldy8, uint8_t* y8t, int64_t ldy8t,
                                 uint32_t* ws, hipStream_t s) {
-    const bool fused = pred && (K % kBK == 0) && ((uintptr_t)A % 16 == 0) && ((uintptr_t)B % 16 == 0) && M > 32 &&
-                       M <= INT32_MAX && N <= INT32_MAX && K < (1 << 22) && (fa == FP8_E4M3 || fa == FP8_E5M2) &&
+    const bool fused = pred && fast_path(A, B, M, N, K) && M > 32 && (fa == FP8_E4M3 || fa == FP8_E5M2) &&
                        fb == FP8_E4M3;
     if (!fused) {  // matmul, then the quantise of its output (same bits, more passes)
         const int32_t st = launch_gemm_nt(A, fa, ba, B, fb, bb, C, FP8_DT_BF16, M, N, K, nullptr, s);
@@ -806,14 +864,28 @@ int32_t launch_gemm_nt(const uint8_t* A, int fa, const int32_t* ba, const uint8_
                        const int32_t* bb, void* C, int out_dt, int64_t M, int64_t N, int64_t K,
                        uint32_t* amax_bits, hipStream_t s) {
     if (amax_bits) hipLaunchKernelGGL(fill_u32_kernel, dim3(1), dim3(64), 0, s, amax_bits, 0u);
-    if (fa == FP8_E4M3 && fb == FP8_E4M3)
-        dispatch_out<FP8_E4M3, FP8_E4M3>(A, ba, B, bb, C, out_dt, M, N, K, amax_bits, s);
-    else if (fa == FP8_E5M2 && fb == FP8_E4M3)
-        dispatch_out<FP8_E5M2, FP8_E4M3>(A, ba, B, bb, C, out_dt, M, N, K, amax_bits, s);
-    else if (fa == FP8_E4M3 && fb == FP8_E5M2)
-        dispatch_out<FP8_E4M3, FP8_E5M2>(A, ba, B, bb, C, out_dt, M, N, K, amax_bits, s);
-    else
-        dispatch_out<FP8_E5M2, FP8_E5M2>(A, ba, B, bb, C, out_dt, M, N, K, amax_bits, s);
+    dispatch_fmts(A, fa, ba, B, fb, bb, C, out_dt, M, N, K, amax_bits != nullptr, amax_bits, BiasOut{}, s);
+    return hip_status();
+}
+
+int32_t launch_gemm_nt_bias(const uint8_t* A, int fa, const int32_t* ba, const uint8_t* B, int fb,
+                            const int32_t* bb, void* C, int out_dt, int64_t M, int64_t N, int64_t K, int bfmt,
+                            int32_t margin, int32_t* bias, uint32_t* amax_bits, uint32_t* flags, uint32_t* ws,
+                            hipStream_t s) {
+    if (fast_path(A, B, M, N, K) && M > 32) {
+        dispatch_fmts(A, fa, ba, B, fb, bb, C, out_dt, M, N, K, true, amax_bits, BiasOut{bias, flags, ws, bfmt, margin}, s);
+        return hip_status();
+    }
+    // decode and fallback kernels: amax with atomics into a zeroed word (ws[0]
+    // if no amax output is wanted, zeroed again afterwards), then the bias
+    uint32_t* acc = amax_bits ? amax_bits : ws;
+    hipLaunchKernelGGL(fill_u32_kernel, dim3(1), dim3(64), 0, s, acc, 0u);
+    dispatch_fmts(A, fa, ba, B, fb, bb, C, out_dt, M, N, K, true, acc, BiasOut{}, s);
+    int32_t st = hip_status();
+    if (st != FP8_OK) return st;
+    st = launch_bias_from_amax(acc, bfmt, margin, bias, flags, s);
+    if (st != FP8_OK || acc != ws) return st;
+    hipLaunchKernelGGL(fill_u32_kernel, dim3(1), dim3(64), 0, s, ws, 0u);
     return hip_status();
 }
 

@@ -58,6 +58,16 @@ int32_t launch_gemm_nt(const uint8_t* A, int fa, const int32_t* ba, const uint8_
                        const int32_t* bb, void* C, int out_dt, int64_t M, int64_t N, int64_t K,
                        uint32_t* amax_bits, hipStream_t s);
 
+// launch_gemm_nt with the epilogue amax of C turned into the Eq. 3 bias for
+// format bfmt in the same launch (256 x 256 kernel: the last workgroup to
+// finish computes it from a running maximum in ws[0..1], which must be zero
+// and is left zero); other kernels: amax with atomics, then the bias kernel.
+// amax_bits and flags may be null.
+int32_t launch_gemm_nt_bias(const uint8_t* A, int fa, const int32_t* ba, const uint8_t* B, int fb,
+                            const int32_t* bb, void* C, int out_dt, int64_t M, int64_t N, int64_t K, int bfmt,
+                            int32_t margin, int32_t* bias, uint32_t* amax_bits, uint32_t* flags, uint32_t* ws,
+                            hipStream_t s);
+
 inline int32_t hip_status() { return hipGetLastError() == hipSuccess ? FP8_OK : FP8_EHIP; }
 
 }  // namespace fp8lin

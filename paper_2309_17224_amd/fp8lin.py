@@ -28,7 +28,8 @@ EXPORTS = (
     "fp8_status_string", "fp8_abi_version", "fp8_scale_bias_ws_bytes", "fp8_scale_bias",
     "fp8_bias_from_amax", "fp8_cast_e4", "fp8_cast_e5", "fp8_cast", "fp8_quantise_ws_bytes",
     "fp8_quantise",
-    "fp8_linear_fwd", "fp8_linear_bwd_dx", "fp8_linear_quantise_ws_bytes",
+    "fp8_linear_fwd", "fp8_linear_bwd_dx", "fp8_linear_bias_ws_bytes", "fp8_linear_fwd_bias",
+    "fp8_linear_bwd_dx_bias", "fp8_linear_quantise_ws_bytes",
     "fp8_linear_fwd_quantise", "fp8_linear_bwd_dx_quantise",
     "fp8_linear_bwd_dw", "ptq_quantise_weights",
 )
@@ -76,6 +77,12 @@ def lib() -> ctypes.CDLL:
             f = getattr(L, name)
             f.restype = i32
             f.argtypes = [vp, vp, vp, vp, vp, i32, i64, i64, i64, vp, vp]
+        L.fp8_linear_bias_ws_bytes.restype = sz
+        L.fp8_linear_bias_ws_bytes.argtypes = []
+        for name in ("fp8_linear_fwd_bias", "fp8_linear_bwd_dx_bias"):
+            f = getattr(L, name)
+            f.restype = i32
+            f.argtypes = [vp, vp, vp, vp, vp, i32, i64, i64, i64, i32, i32, vp, vp, vp, vp, sz, vp]
         L.fp8_linear_quantise_ws_bytes.restype = sz
         L.fp8_linear_quantise_ws_bytes.argtypes = [i64, i64]
         for name in ("fp8_linear_fwd_quantise", "fp8_linear_bwd_dx_quantise"):
@@ -266,6 +273,48 @@ def fp8_linear_bwd_dx(dy8, bg, w8, bw, out_dt=DT_BF16, dx=None, dx_amax_bits=Non
                                  _p(dx_amax_bits), _stream(stream))
     _check("fp8_linear_bwd_dx", st)
     return dx
+
+
+def bias_workspace(device) -> torch.Tensor:
+    """Workspace of fp8_linear_fwd_bias / fp8_linear_bwd_dx_bias: zeros, and
+    left zero by every completed call (one per stream of concurrent calls)."""
+    return torch.zeros(int(lib().fp8_linear_bias_ws_bytes()) // 4, dtype=torch.int32, device=device)
+
+
+def _gemm_bias(name, a8, ba, b8, bb, out, out_dt, rows, cols, kc, fmt, margin, bias, amax_bits, flags,
+               ws, stream):
+    dev = a8.device
+    out = _out((rows, cols), out_dt, dev, out)
+    bias = _i32(dev) if bias is None else bias
+    amax_bits = _i32(dev) if amax_bits is None else amax_bits
+    flags = _i32(dev) if flags is None else flags
+    ws = bias_workspace(dev) if ws is None else ws
+    st = getattr(lib(), name)(_p(a8), _p(ba), _p(b8), _p(bb), _p(out), _odt(out_dt, out), *(
+        (rows, cols, kc) if name == "fp8_linear_fwd_bias" else (rows, kc, cols)),
+        fmt, margin, _p(bias), _p(amax_bits), _p(flags), _p(ws), ws.numel() * ws.element_size(),
+        _stream(stream))
+    _check(name, st)
+    return out, bias, amax_bits, flags
+
+
+def fp8_linear_fwd_bias(x8, bx, w8t, bw, fmt=E4M3, margin=0, out_dt=DT_BF16, y=None, bias=None,
+                        amax_bits=None, flags=None, ws=None, stream=None):
+    """Y = fp8_linear_fwd(...) with the Eq. 3 bias of Y (format fmt) from the
+    same launch.  Returns (y, bias, amax_bits, flags)."""
+    M, K = x8.shape
+    N = w8t.shape[0]
+    return _gemm_bias("fp8_linear_fwd_bias", x8, bx, w8t, bw, y, out_dt, M, N, K, fmt, margin, bias,
+                      amax_bits, flags, ws, stream)
+
+
+def fp8_linear_bwd_dx_bias(dy8, bg, w8, bw, fmt=E5M2, margin=0, out_dt=DT_BF16, dx=None, bias=None,
+                           amax_bits=None, flags=None, ws=None, stream=None):
+    """dX = fp8_linear_bwd_dx(...) with the Eq. 3 bias of dX from the same
+    launch.  Returns (dx, bias, amax_bits, flags)."""
+    M, N = dy8.shape
+    K = w8.shape[0]
+    return _gemm_bias("fp8_linear_bwd_dx_bias", dy8, bg, w8, bw, dx, out_dt, M, K, N, fmt, margin, bias,
+                      amax_bits, flags, ws, stream)
 
 
 def _gemm_quantise(name, a8, ba, b8, bb, out, rows, cols, kc, fmt, margin, bias_pred, bias,

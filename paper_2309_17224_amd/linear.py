@@ -177,14 +177,18 @@ class WorkloadStep:
       "cscale":    FP8-CSCALE (Sec. 3): one constant bias `cscale_bias` for every
                    weight, activation and gradient; no amax, only the casts and
                    the matmuls (no epilogue amax either).
+    fused_bias: the forward and grad-input matmuls take the bias of their
+      outputs in the same launch (fp8_linear_fwd_bias / fp8_linear_bwd_dx_bias);
+      False: epilogue amax, then fp8_bias_from_amax (identical bits).
     """
 
     QUANT_MODES = ("predicted", "twopass", "separate", "cscale")
 
     def __init__(self, workload, tensors: dict, device, margin: int = 0, quant: str = "predicted",
-                 cscale_bias: int = 0):
+                 cscale_bias: int = 0, fused_bias: bool = True):
         if quant not in self.QUANT_MODES:
             raise ValueError(f"quant must be one of {self.QUANT_MODES}")
+        self.fused_bias = bool(fused_bias)
         self.w = workload
         self.t = tensors
         self.dev = torch.device(device)
@@ -196,6 +200,7 @@ class WorkloadStep:
         self.ws = F.workspace(nmax, device)
         qws = max(F.fp8_quantise_ws_bytes(*x.shape) for x in tensors.values())
         self.qws = torch.empty(max(qws, 4), dtype=torch.uint8, device=device)
+        self.bws = F.bias_workspace(device)  # the step's matmuls run one after another
         self.q = {}
         train = workload.train
         for l in lin:
@@ -267,6 +272,13 @@ class WorkloadStep:
             if l.M <= 32:
                 kind, work = "gemm_decode", l.N * l.K + l.M * l.K + 2 * l.M * l.N
             amax_y = self.w.train and self.quant != "cscale"
+            if amax_y and self.fused_bias:
+                calls.append((f"fwd {l.name}", kind, work,
+                              lambda xq=xq, wq=wq, o=o: F.fp8_linear_fwd_bias(
+                                  xq.q, xq.bias, wq.qT, wq.bias, F.E4M3, 0, y=o["y"],
+                                  bias=o["y_scal"][0:1], amax_bits=o["y_scal"][1:2],
+                                  flags=o["y_scal"][2:3], ws=self.bws)))
+                continue
             calls.append((f"fwd {l.name}", kind, work,
                           lambda xq=xq, wq=wq, o=o, amax_y=amax_y: F.fp8_linear_fwd(
                               xq.q, xq.bias, wq.qT, wq.bias, y=o["y"],
@@ -285,11 +297,18 @@ class WorkloadStep:
                 xq, wq, gq, o = self.q[l.x], self.q[l.w], self.q[l.dy], self.out[l.name]
                 flop = 2 * l.M * l.N * l.K
                 amax_dx = self.quant != "cscale"
-                calls.append((f"dx {l.name}", "gemm_dx", flop,
-                              lambda wq=wq, gq=gq, o=o, amax_dx=amax_dx: F.fp8_linear_bwd_dx(
-                                  gq.q, gq.bias, wq.q, wq.bias, dx=o["dx"],
-                                  dx_amax_bits=o["dx_scal"][1:2] if amax_dx else None)))
-                if amax_dx:
+                if amax_dx and self.fused_bias:
+                    calls.append((f"dx {l.name}", "gemm_dx", flop,
+                                  lambda wq=wq, gq=gq, o=o: F.fp8_linear_bwd_dx_bias(
+                                      gq.q, gq.bias, wq.q, wq.bias, F.E5M2, self.margin, dx=o["dx"],
+                                      bias=o["dx_scal"][0:1], amax_bits=o["dx_scal"][1:2],
+                                      flags=o["dx_scal"][2:3], ws=self.bws)))
+                else:
+                    calls.append((f"dx {l.name}", "gemm_dx", flop,
+                                  lambda wq=wq, gq=gq, o=o, amax_dx=amax_dx: F.fp8_linear_bwd_dx(
+                                      gq.q, gq.bias, wq.q, wq.bias, dx=o["dx"],
+                                      dx_amax_bits=o["dx_scal"][1:2] if amax_dx else None)))
+                if amax_dx and not self.fused_bias:
                     calls.append((f"bias dx {l.name}", "bias", 0,
                                   lambda o=o: F.fp8_bias_from_amax(o["dx_scal"][1:2], F.E5M2,
                                                                    self.margin, bias=o["dx_scal"][0:1],

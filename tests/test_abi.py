@@ -137,3 +137,21 @@ def test_ptq_and_bias_from_amax_reject(L):
     assert L.fp8_bias_from_amax(NULL, 0, 0, FAKE, NULL, NULL) == F.EINVAL
     assert L.fp8_bias_from_amax(FAKE, 5, 0, FAKE, NULL, NULL) == F.EINVAL
     assert L.fp8_bias_from_amax(FAKE, 0, 0, ODD, NULL, NULL) == F.EINVAL
+
+
+def test_gemm_bias_rejects(L):
+    assert L.fp8_linear_bias_ws_bytes() == 8
+    for f in (L.fp8_linear_fwd_bias, L.fp8_linear_bwd_dx_bias):
+        # (a, ba, b, bb, c, c_dt, M, N, K, fmt, margin, bias, amax, flags, ws, ws_bytes, stream)
+        assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 3, 4, 4, 4, 0, 0, FAKE, NULL, NULL, FAKE, 8, NULL) == F.EINVAL   # dtype
+        assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 0, 4, 4, 4, 4, 0, FAKE, NULL, NULL, FAKE, 8, NULL) == F.EINVAL   # format
+        assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 0, 4, 4, 4, 0, 1 << 20, FAKE, NULL, NULL, FAKE, 8, NULL) == F.EINVAL  # margin
+        assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 0, 4, 4, 4, 0, 0, NULL, NULL, NULL, FAKE, 8, NULL) == F.EINVAL   # bias
+        assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 0, 4, 4, 4, 0, 0, FAKE, NULL, NULL, NULL, 8, NULL) == F.EINVAL   # ws
+        assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 0, 4, 4, 4, 0, 0, FAKE, NULL, NULL, FAKE, 4, NULL) == F.EINVAL   # ws small
+        assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 0, 4, 4, 4, 0, 0, FAKE, NULL, NULL, ODD, 8, NULL) == F.EINVAL    # ws align
+        assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 0, 4, 4, 4, 0, 0, FAKE, ODD, NULL, FAKE, 8, NULL) == F.EINVAL    # amax align
+        assert f(NULL, FAKE, FAKE, FAKE, FAKE, 0, 4, 4, 4, 0, 0, FAKE, NULL, NULL, FAKE, 8, NULL) == F.EINVAL   # operand
+        assert f(FAKE, FAKE, FAKE, FAKE, NULL, 0, 4, 4, 4, 0, 0, FAKE, NULL, NULL, FAKE, 8, NULL) == F.EINVAL   # output
+        assert f(FAKE, FAKE, FAKE, FAKE, ODD, 0, 4, 4, 4, 0, 0, FAKE, NULL, NULL, FAKE, 8, NULL) == F.EINVAL    # out align
+        assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 0, -1, 4, 4, 0, 0, FAKE, NULL, NULL, FAKE, 8, NULL) == F.EINVAL  # M < 0
