@@ -37,8 +37,8 @@ DEFAULT_WORKLOAD = "llama2-7b-up"
 def parse():
     p = argparse.ArgumentParser(description=__doc__)
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=20)
-    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--workload", default=DEFAULT_WORKLOAD)
     p.add_argument("--margin", type=int, default=0)
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -52,6 +52,10 @@ def parse():
                         "fp8_quantise without prediction, fp8_scale_bias + fp8_cast, or FP8-CSCALE "
                         "(constant bias --cscale-bias, no amax: not the headline metric)")
     p.add_argument("--cscale-bias", type=int, default=0)
+    p.add_argument("--streams", type=int, choices=(1, 2), default=1,
+                   help="graph of the timed steps: independent calls (input quantises, gradient "
+                        "quantises, each linear's grad-input and grad-weight matmuls) on two "
+                        "streams, or everything on one")
     p.add_argument("--bias", choices=("fused", "separate"), default="fused",
                    help="bias of Y and dX: taken by the matmul launch itself (last workgroup), "
                         "or epilogue amax + fp8_bias_from_amax (identical bits)")
@@ -276,7 +280,8 @@ def main():
     tens = {k: v.to(dev) for k, v in cpu.items()}
     torch.cuda.synchronize()
     step = L.WorkloadStep(w, tens, dev, margin=args.margin, quant=args.quant,
-                          cscale_bias=args.cscale_bias, fused_bias=args.bias == "fused")
+                          cscale_bias=args.cscale_bias, fused_bias=args.bias == "fused",
+                          concurrent=args.streams == 2)
     if not w.train:
         step.prepare_inference()
     flush = None
@@ -309,8 +314,8 @@ def main():
                    "accumulate": "fp32", "outputs": "Y,dX bf16; dW fp32",
                    "margin": args.margin, "mall_flush_mb": args.flush_mb, "quant": args.quant,
                    "output_bias": args.bias,
-                   "launch": "one HIP graph replay per step" if args.launch == "graph"
-                   else "one host call per library call"},
+                   "launch": (f"one HIP graph replay per step, {args.streams} stream(s)" if args.launch == "graph"
+                              else "one host call per library call")},
         "frac_of_fp8_peak": round(value / FP8_PEAK_TFLOPS, 4),
         "roofline": roof,
         "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv) for kk, vv in d.items()}

@@ -18,6 +18,7 @@ Every buffer is allocated once, up front; a step launches kernels only.
 """
 from __future__ import annotations
 
+import gc
 from dataclasses import dataclass
 
 import torch
@@ -147,6 +148,7 @@ class Fp8Tensor:
         self.q = torch.empty((rows, cols), **u8) if want_q else None
         self.qT = torch.empty((cols, rows), **u8) if want_qT else None
         self.scal = torch.zeros(3, dtype=torch.int32, device=device)
+        self.qws = self.sws = None  # quantise / scale-bias workspaces (set by the step)
 
     @property
     def bias(self): return self.scal[0:1]
@@ -180,12 +182,20 @@ class WorkloadStep:
     fused_bias: the forward and grad-input matmuls take the bias of their
       outputs in the same launch (fp8_linear_fwd_bias / fp8_linear_bwd_dx_bias);
       False: epilogue amax, then fp8_bias_from_amax (identical bits).
+    concurrent: capture() records independent calls on two streams (the
+      quantise calls of the weights and activations, those of the gradients,
+      and each linear's grad-input and grad-weight matmuls), so that the last
+      partial round of workgroups of one kernel can overlap the other; run()
+      always issues the calls one after another.  Same bits either way.  Off
+      by default: on the measured workloads it gained nothing (the paired
+      matmuls still need the same number of rounds of workgroups) and cost 3 %
+      on the Llama-2-70B MLP step (operand panels of two kernels share L2).
     """
 
     QUANT_MODES = ("predicted", "twopass", "separate", "cscale")
 
     def __init__(self, workload, tensors: dict, device, margin: int = 0, quant: str = "predicted",
-                 cscale_bias: int = 0, fused_bias: bool = True):
+                 cscale_bias: int = 0, fused_bias: bool = True, concurrent: bool = False):
         if quant not in self.QUANT_MODES:
             raise ValueError(f"quant must be one of {self.QUANT_MODES}")
         self.fused_bias = bool(fused_bias)
@@ -198,9 +208,6 @@ class WorkloadStep:
         lin = workload.linears
         nmax = max(x.numel() for x in tensors.values())
         self.ws = F.workspace(nmax, device)
-        qws = max(F.fp8_quantise_ws_bytes(*x.shape) for x in tensors.values())
-        self.qws = torch.empty(max(qws, 4), dtype=torch.uint8, device=device)
-        self.bws = F.bias_workspace(device)  # the step's matmuls run one after another
         self.q = {}
         train = workload.train
         for l in lin:
@@ -220,6 +227,16 @@ class WorkloadStep:
                          dw=torch.empty((l.K, l.N), dtype=torch.float32, device=device),
                          dx_scal=torch.zeros(3, dtype=torch.int32, device=device))
             self.out[l.name] = o
+        # bias workspaces of the forward and grad-input matmuls (zero between calls)
+        self.bws = {l.name: F.bias_workspace(device) for l in lin}
+        # a workspace per tensor: calls on different streams never share one
+        for name, qt in self.q.items():
+            x = tensors[name]
+            qt.qws = torch.empty(max(F.fp8_quantise_ws_bytes(*x.shape), 4), dtype=torch.uint8, device=device)
+            qt.sws = F.workspace(x.numel(), device)
+        self.concurrent = bool(concurrent) and self.dev.type == "cuda"
+        self.side = torch.cuda.Stream(self.dev) if self.concurrent else None  # default priority
+        self.sched = []
         self.calls = self._build()
 
     def _quant(self, name, fmt, margin):
@@ -240,28 +257,39 @@ class WorkloadStep:
                      lambda: F.fp8_quantise(x, fmt, margin, bias_pred=pred, bias=qt.bias,
                                             amax_bits=qt.amax, flags=qt.flags, q=qt.q, qT=qt.qT,
                                             want_q=qt.q is not None, want_qT=qt.qT is not None,
-                                            ws=self.qws))]
+                                            ws=qt.qws))]
         return [
             (f"amax+bias {name}", "amax", 2 * n,
              lambda: F.fp8_scale_bias(x, fmt, margin, bias=qt.bias, amax_bits=qt.amax,
-                                      flags=qt.flags, ws=self.ws)),
+                                      flags=qt.flags, ws=qt.sws)),
             (f"cast {name}", "cast", 3 * n + (n if qt.qT is not None and qt.q is not None else 0),
              lambda: cast(x, qt.bias, q=qt.q, qT=qt.qT, want_q=qt.q is not None,
                           want_qT=qt.qT is not None)),
         ]
 
     def _build(self):
-        calls = []
+        """The step's calls in issue order; self.sched[i] = (phase, branch) of
+        call i: consecutive calls of one phase are independent across branches
+        (phase None: on its own)."""
+        calls, sched = [], []
+
+        def add(cs, phase=None, branch=0):
+            calls.extend(cs)
+            sched.extend([(phase, branch)] * len(cs))
+
         lin = self.w.linears
         done = set()
         weights = [l.w for l in lin]
+        nq = 0
         if self.w.train:
             for name in dict.fromkeys(weights):
-                calls += self._quant(name, F.E4M3, 0)
+                add(self._quant(name, F.E4M3, 0), "quantise inputs", nq % 2)
+                nq += 1
                 done.add(name)
         for l in lin:
             if l.x not in done:
-                calls += self._quant(l.x, F.E4M3, 0)
+                add(self._quant(l.x, F.E4M3, 0), "quantise inputs", nq % 2)
+                nq += 1
                 done.add(l.x)
         for l in lin:
             xq, wq, o = self.q[l.x], self.q[l.w], self.out[l.name]
@@ -273,49 +301,53 @@ class WorkloadStep:
                 kind, work = "gemm_decode", l.N * l.K + l.M * l.K + 2 * l.M * l.N
             amax_y = self.w.train and self.quant != "cscale"
             if amax_y and self.fused_bias:
-                calls.append((f"fwd {l.name}", kind, work,
-                              lambda xq=xq, wq=wq, o=o: F.fp8_linear_fwd_bias(
-                                  xq.q, xq.bias, wq.qT, wq.bias, F.E4M3, 0, y=o["y"],
-                                  bias=o["y_scal"][0:1], amax_bits=o["y_scal"][1:2],
-                                  flags=o["y_scal"][2:3], ws=self.bws)))
+                add([(f"fwd {l.name}", kind, work,
+                      lambda xq=xq, wq=wq, o=o, bws=self.bws[l.name]: F.fp8_linear_fwd_bias(
+                          xq.q, xq.bias, wq.qT, wq.bias, F.E4M3, 0, y=o["y"],
+                          bias=o["y_scal"][0:1], amax_bits=o["y_scal"][1:2],
+                          flags=o["y_scal"][2:3], ws=bws))])
                 continue
-            calls.append((f"fwd {l.name}", kind, work,
-                          lambda xq=xq, wq=wq, o=o, amax_y=amax_y: F.fp8_linear_fwd(
-                              xq.q, xq.bias, wq.qT, wq.bias, y=o["y"],
-                              y_amax_bits=o["y_scal"][1:2] if amax_y else None)))
+            add([(f"fwd {l.name}", kind, work,
+                  lambda xq=xq, wq=wq, o=o, amax_y=amax_y: F.fp8_linear_fwd(
+                      xq.q, xq.bias, wq.qT, wq.bias, y=o["y"],
+                      y_amax_bits=o["y_scal"][1:2] if amax_y else None))])
             if amax_y:
-                calls.append((f"bias y {l.name}", "bias", 0,
-                              lambda o=o: F.fp8_bias_from_amax(o["y_scal"][1:2], F.E4M3, 0,
-                                                               bias=o["y_scal"][0:1],
-                                                               flags=o["y_scal"][2:3])))
+                add([(f"bias y {l.name}", "bias", 0,
+                      lambda o=o: F.fp8_bias_from_amax(o["y_scal"][1:2], F.E4M3, 0,
+                                                       bias=o["y_scal"][0:1],
+                                                       flags=o["y_scal"][2:3]))])
         if self.w.train:
+            nq = 0
             for l in lin:
                 if l.dy not in done:
-                    calls += self._quant(l.dy, F.E5M2, self.margin)
+                    add(self._quant(l.dy, F.E5M2, self.margin), "quantise gradients", nq % 2)
+                    nq += 1
                     done.add(l.dy)
             for l in lin:
                 xq, wq, gq, o = self.q[l.x], self.q[l.w], self.q[l.dy], self.out[l.name]
                 flop = 2 * l.M * l.N * l.K
                 amax_dx = self.quant != "cscale"
+                ph = f"backward {l.name}"
                 if amax_dx and self.fused_bias:
-                    calls.append((f"dx {l.name}", "gemm_dx", flop,
-                                  lambda wq=wq, gq=gq, o=o: F.fp8_linear_bwd_dx_bias(
-                                      gq.q, gq.bias, wq.q, wq.bias, F.E5M2, self.margin, dx=o["dx"],
-                                      bias=o["dx_scal"][0:1], amax_bits=o["dx_scal"][1:2],
-                                      flags=o["dx_scal"][2:3], ws=self.bws)))
+                    add([(f"dx {l.name}", "gemm_dx", flop,
+                          lambda wq=wq, gq=gq, o=o, bws=self.bws[l.name], mg=self.margin: F.fp8_linear_bwd_dx_bias(
+                              gq.q, gq.bias, wq.q, wq.bias, F.E5M2, mg, dx=o["dx"],
+                              bias=o["dx_scal"][0:1], amax_bits=o["dx_scal"][1:2],
+                              flags=o["dx_scal"][2:3], ws=bws))], ph, 0)
                 else:
-                    calls.append((f"dx {l.name}", "gemm_dx", flop,
-                                  lambda wq=wq, gq=gq, o=o, amax_dx=amax_dx: F.fp8_linear_bwd_dx(
-                                      gq.q, gq.bias, wq.q, wq.bias, dx=o["dx"],
-                                      dx_amax_bits=o["dx_scal"][1:2] if amax_dx else None)))
+                    add([(f"dx {l.name}", "gemm_dx", flop,
+                          lambda wq=wq, gq=gq, o=o, amax_dx=amax_dx: F.fp8_linear_bwd_dx(
+                              gq.q, gq.bias, wq.q, wq.bias, dx=o["dx"],
+                              dx_amax_bits=o["dx_scal"][1:2] if amax_dx else None))], ph, 0)
                 if amax_dx and not self.fused_bias:
-                    calls.append((f"bias dx {l.name}", "bias", 0,
-                                  lambda o=o: F.fp8_bias_from_amax(o["dx_scal"][1:2], F.E5M2,
-                                                                   self.margin, bias=o["dx_scal"][0:1],
-                                                                   flags=o["dx_scal"][2:3])))
-                calls.append((f"dw {l.name}", "gemm_dw", flop,
-                              lambda xq=xq, gq=gq, o=o: F.fp8_linear_bwd_dw(
-                                  xq.qT, xq.bias, gq.qT, gq.bias, dw=o["dw"])))
+                    add([(f"bias dx {l.name}", "bias", 0,
+                          lambda o=o, mg=self.margin: F.fp8_bias_from_amax(o["dx_scal"][1:2], F.E5M2,
+                                                                           mg, bias=o["dx_scal"][0:1],
+                                                           flags=o["dx_scal"][2:3]))], ph, 0)
+                add([(f"dw {l.name}", "gemm_dw", flop,
+                      lambda xq=xq, gq=gq, o=o: F.fp8_linear_bwd_dw(
+                          xq.qT, xq.bias, gq.qT, gq.bias, dw=o["dw"]))], ph, 1)
+        self.sched = sched
         return calls
 
     def prepare_inference(self):
@@ -329,16 +361,62 @@ class WorkloadStep:
         for _, _, _, fn in self.calls:
             fn()
 
+    def run_concurrent(self):
+        """The step with independent calls forked onto the side stream: for
+        each phase, branch-1 calls run on the side stream after an event of
+        the current stream, and the current stream waits for them before the
+        next phase."""
+        main = torch.cuda.current_stream(self.dev)
+        i, n = 0, len(self.calls)
+        while i < n:
+            phase = self.sched[i][0]
+            j = i + 1
+            while phase is not None and j < n and self.sched[j][0] == phase:
+                j += 1
+            group = range(i, j)
+            if all(self.sched[k][1] == 0 for k in group):
+                for k in group:
+                    self.calls[k][3]()
+            else:
+                fork = torch.cuda.Event()
+                fork.record(main)
+                self.side.wait_event(fork)
+                for k in group:
+                    if self.sched[k][1] == 0:
+                        self.calls[k][3]()
+                with torch.cuda.stream(self.side):
+                    for k in group:
+                        if self.sched[k][1] != 0:
+                            self.calls[k][3]()
+                join = torch.cuda.Event()
+                join.record(self.side)
+                main.wait_event(join)
+            i = j
+
     def capture(self):
-        """Record one step (every call, in order) into a HIP graph, so that
-        replay() launches the whole step with one host call.  The library
-        launches only kernels (no memset or copy nodes) on the current stream,
-        and every buffer is allocated beforehand, so replays recompute the
-        step from the current contents of the input tensors."""
+        """Record one step into a HIP graph, so that replay() launches the
+        whole step with one host call (independent calls on two streams when
+        concurrent).  The library launches only kernels (no memset or copy
+        nodes) on the current stream, and every buffer is allocated
+        beforehand, so replays recompute the step from the current contents of
+        the input tensors."""
         torch.cuda.synchronize(self.dev)
         g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            self.run()
+        # Dead objects that own HIP resources (an earlier step's graph) must
+        # not be destroyed while the stream is capturing: collect them now and
+        # keep the cyclic collector off until the capture ends.
+        gc.collect()
+        was_enabled = gc.isenabled()
+        gc.disable()
+        try:
+            with torch.cuda.graph(g):
+                if self.concurrent:
+                    self.run_concurrent()
+                else:
+                    self.run()
+        finally:
+            if was_enabled:
+                gc.enable()
         torch.cuda.synchronize(self.dev)
         self.graph = g
         return g
