@@ -14,6 +14,10 @@ Paper passages (section / equation / table):
   * ``gemm_nt``: Sec. 2 and 2.2 (FP8 x FP8, high-precision accumulate),
     Sec. 2.1 Eq. 2 (unscale by -(b_a + b_b))
   * ``ptq_quantise_weights``: Sec. 3.1
+  * ``quantise_segments``, ``gemm_nt_rows``: one bias per micro batch / data or
+    tensor replica (Sec. 4) and per data sample at inference (App. D): each
+    row segment is an independent tensor for ``scale_bias`` and ``cast``
+  * ``bias_mode``: the statistical mode of per-sample biases (App. D, App. F)
 """
 from __future__ import annotations
 
@@ -194,6 +198,52 @@ def ptq_quantise_weights(w: np.ndarray):
     if st:
         raise ValueError("oracle_ptq_quantise_weights failed")
     return w8, w8t, int(b.value), int(fl.value)
+
+
+def quantise_segments(x: np.ndarray, offsets, fmt: int, margin: int = 0):
+    """Rows offsets[s] .. offsets[s+1]-1 of x form segment s, quantised as a
+    tensor of its own: returns (q, qT, biases, amax bits, flags, row_bias)."""
+    x, dt = _hp(x)
+    rows, cols = x.shape
+    q = np.zeros((rows, cols), dtype=np.uint8)
+    qT = np.zeros((cols, rows), dtype=np.uint8)
+    row_bias = np.zeros(rows, dtype=np.int32)
+    biases, amaxes, flags = [], [], []
+    for s in range(len(offsets) - 1):
+        lo, hi = int(offsets[s]), int(offsets[s + 1])
+        seg = x[lo:hi]
+        b, a, fl = scale_bias(seg.reshape(-1), fmt, margin)
+        biases.append(b)
+        amaxes.append(a)
+        flags.append(fl)
+        row_bias[lo:hi] = b
+        if hi > lo and cols > 0:
+            q[lo:hi] = cast(seg, fmt, b)
+            qT[:, lo:hi] = q[lo:hi].T
+    return q, qT, biases, amaxes, flags, row_bias
+
+
+def gemm_nt_rows(a8: np.ndarray, fmt_a: int, ba_rows, b8: np.ndarray, fmt_b: int, bb: int,
+                 out_dt: int = F32) -> np.ndarray:
+    """gemm_nt with one bias per row of a8: row m unscaled by 2^-(ba_rows[m] + bb)."""
+    ba_rows = np.asarray(ba_rows, dtype=np.int64)
+    M, N = a8.shape[0], b8.shape[0]
+    out = np.empty((M, N), dtype=np.float32 if out_dt == F32 else np.uint16)
+    for v in np.unique(ba_rows):
+        rows = np.nonzero(ba_rows == v)[0]
+        out[rows] = gemm_nt(a8, fmt_a, int(v), b8, fmt_b, bb, out_dt=out_dt, rows=rows)
+    return out
+
+
+def bias_mode(biases) -> int:
+    """The most frequent bias, the smallest of equally frequent ones; a bias is
+    counted clamped to [-1024, 1023] (the range the library's histogram holds)."""
+    counts: dict[int, int] = {}
+    for b in biases:
+        v = max(-1024, min(1023, int(b)))
+        counts[v] = counts.get(v, 0) + 1
+    top = max(counts.values())
+    return min(v for v, c in counts.items() if c == top)
 
 
 def bf16_to_f64(h: int) -> float:
