@@ -184,6 +184,53 @@ int32_t fp8_quantise(const void *x, int32_t dt, int64_t rows, int64_t cols, int6
                      uint8_t *qT, int64_t ldqT, void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * fp8_quantise_segments -- FP8-AMAX for every row segment of one tensor in one
+ * call: the paper takes a bias per micro-batch and per data or tensor replica
+ * (Sec. 4), and per data sample at inference (the per-sample activation biases
+ * whose mode App. D and F plot).  Rows offsets[s] <= r < offsets[s+1] form
+ * segment s; each segment gets its own amax, Eq. 3 bias (format fmt, margin)
+ * and flags, and its rows are cast with its bias.
+ * x:         [rows, cols] of type dt, row stride ldx >= cols.
+ * offsets:   device int32 [nseg + 1], nondecreasing from 0 to rows (read on
+ *            the device; other contents give unspecified biases and codes but
+ *            never an access out of bounds).  nseg >= 1.
+ * bias, amax_bits: out, device [nseg]; flags: out, optional, [nseg].
+ * row_bias:  out, device int32 [rows]: the bias of each row's segment (the
+ *            per-row bias of fp8_linear_fwd_rows).
+ * q, qT:     out, optional: codes [rows, cols] (row stride ldq) and
+ *            transposed codes [cols, rows] (row stride ldqT).
+ * An empty segment has amax 0, bias 0 and FP8_FLAG_ZERO.
+ */
+int32_t fp8_quantise_segments(const void *x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx, int32_t fmt,
+                              int32_t margin, const int32_t *offsets, int64_t nseg, int32_t *bias,
+                              uint32_t *amax_bits, uint32_t *flags, int32_t *row_bias, uint8_t *q, int64_t ldq,
+                              uint8_t *qT, int64_t ldqT, void *stream);
+
+/*
+ * fp8_linear_fwd_rows -- the forward matmul of fp8_linear_fwd with one
+ * activation bias per row (per data sample, Sec. 3.1 inference with the
+ * activation bias of each sample):
+ *   Y[m, n] = 2^-(bx_rows[m] + bw) * sum_k X8[m, k] * W8[k, n]
+ * bx_rows: device int32 [M] (row_bias of fp8_quantise_segments).  The other
+ * arguments are those of fp8_linear_fwd.
+ */
+int32_t fp8_linear_fwd_rows(const uint8_t *x8, const int32_t *bx_rows, const uint8_t *w8t, const int32_t *bw,
+                            void *y, int32_t y_dt, int64_t M, int64_t N, int64_t K, uint32_t *y_amax_bits,
+                            void *stream);
+
+/*
+ * fp8_bias_mode -- bias telemetry (App. D and F plot the statistical mode of
+ * the per-sample biases of a batch, step by step): the mode of bias[0..n)
+ * (the most frequent value; the smallest of equally frequent ones; a bias
+ * below -1024 counts as -1024, one above 1023 as 1023) is written to
+ * ring[*count % capacity], then *count is incremented, all on the device, so
+ * a captured graph keeps appending.  n == 0 is a no-op.
+ * ring: device int32 [capacity], capacity >= 1.  count: device uint32.
+ */
+int32_t fp8_bias_mode(const int32_t *bias, int64_t n, int32_t *ring, int64_t capacity, uint32_t *count,
+                      void *stream);
+
+/*
  * fp8_linear_fwd -- forward FP8 matmul with unscale (Sec. 2, Eq. 2):
  *   Y[m, n] = 2^-(bx + bw) * sum_k X8[m, k] * W8[k, n]
  * x8:  [M, K] E4M3 codes (dense), bias *bx.

@@ -115,17 +115,22 @@ __device__ __forceinline__ uint32_t byte_of(uint32_t w, int j) { return (w >> (8
 // reduction by the caller.  Every thread of the block must call it (it
 // synchronises through the LDS tile), and it leaves the LDS tile free for
 // the next call.
-template <int DT, int FMT, bool MAX>
+// With ROWB, row r is cast with its own bias rowb[r] (clamped) instead of b.
+template <int DT, int FMT, bool MAX, bool ROWB = false>
 __device__ __forceinline__ uint32_t cast_tile(const void* __restrict__ x, int64_t rows, int64_t cols,
                                               int64_t ldx, int b, uint8_t* __restrict__ q, int64_t ldq,
                                               uint8_t* __restrict__ qT, int64_t ldqT, int64_t tr,
                                               int64_t tc, int vec_in, int vec_q, int vec_qT,
-                                              uint8_t* __restrict__ tile) {
+                                              uint8_t* __restrict__ tile,
+                                              const int32_t* __restrict__ rowb = nullptr) {
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int chunk = lane & 15, g = lane >> 4;
     const int64_t R0 = tr * kCastRows, C0 = tc * kCastCols;
     const int lr = (w * 4 + g) * kRpt, lc = chunk * 8;
     const int64_t r0 = R0 + lr, c0 = C0 + lc;
+    int bi[kRpt];  // bias of each of this lane's rows
+#pragma unroll
+    for (int i = 0; i < kRpt; ++i) bi[i] = ROWB ? (r0 + i < rows ? clamp_bias(rowb[r0 + i]) : 0) : b;
 
     uint32_t lo[kRpt], hi[kRpt];  // codes of columns c0..c0+3 and c0+4..c0+7, per row
     uint32_t mag = 0;
@@ -143,8 +148,8 @@ __device__ __forceinline__ uint32_t cast_tile(const void* __restrict__ x, int64_
             }
 #pragma unroll
             for (int i = 0; i < kRpt; ++i) {
-                lo[i] = cast4_bf16<FMT>(v[i].x, v[i].y, b);
-                hi[i] = cast4_bf16<FMT>(v[i].z, v[i].w, b);
+                lo[i] = cast4_bf16<FMT>(v[i].x, v[i].y, bi[i]);
+                hi[i] = cast4_bf16<FMT>(v[i].z, v[i].w, bi[i]);
                 if (__builtin_expect(any_nan_bf16(v[i].x, v[i].y) || any_nan_bf16(v[i].z, v[i].w), 0)) {
                     const uint32_t h0[4] = {v[i].x & 0xFFFFu, v[i].x >> 16, v[i].y & 0xFFFFu, v[i].y >> 16};
                     const uint32_t h1[4] = {v[i].z & 0xFFFFu, v[i].z >> 16, v[i].w & 0xFFFFu, v[i].w >> 16};
@@ -158,8 +163,8 @@ __device__ __forceinline__ uint32_t cast_tile(const void* __restrict__ x, int64_
                 const uint4* p = (const uint4*)((const uint32_t*)x + (r0 + i) * ldx + c0);
                 const uint4 a = ld_stream(p), bb = ld_stream(p + 1);
                 if (MAX) mag = fold_f32(fold_f32(mag, a), bb);
-                lo[i] = cast4_f32<FMT>(a, b);
-                hi[i] = cast4_f32<FMT>(bb, b);
+                lo[i] = cast4_f32<FMT>(a, bi[i]);
+                hi[i] = cast4_f32<FMT>(bb, bi[i]);
                 const uint32_t m = (a.x | a.y | a.z | a.w | bb.x | bb.y | bb.z | bb.w) & 0x7F800000u;
                 if (__builtin_expect(m == 0x7F800000u, 0)) {  // some exponent field may be all ones
                     const uint32_t h0[4] = {f32_key(a.x), f32_key(a.y), f32_key(a.z), f32_key(a.w)};
@@ -177,7 +182,7 @@ __device__ __forceinline__ uint32_t cast_tile(const void* __restrict__ x, int64_
                 const int64_t r = r0 + i, c = c0 + j;
                 uint32_t code = 0u;
                 if (r < rows && c < cols) {
-                    code = cast1<DT, FMT>(x, r * ldx + c, b);
+                    code = cast1<DT, FMT>(x, r * ldx + c, bi[i]);
                     if (MAX) mag = max(mag, elem_mag<DT>(x, r * ldx + c));
                 }
                 if (j < 4) wlo |= code << (8 * j); else whi |= code << (8 * (j - 4));
@@ -392,6 +397,169 @@ void with_dt_fmt(int dt, int fmt, Fn&& fn) {
         with_fmt(fmt, [&](auto F) { fn(IC<FP8_DT_F32>{}, F); });
 }
 
+
+// ------------------------------------------- segments: one bias per row group
+// Segment s holds rows offsets[s] <= r < offsets[s + 1] (one data sample or
+// micro-batch).  seg_of(r) is the largest s < nseg with offsets[s] <= r (0 if
+// none), so every index stays in [0, nseg) whatever the offsets hold: invalid
+// offsets give unspecified biases, never an access out of bounds.
+__device__ __forceinline__ int seg_of(const int32_t* __restrict__ off, int nseg, int64_t r) {
+    int lo = 0, hi = nseg - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if ((int64_t)off[mid] <= r) lo = mid; else hi = mid - 1;
+    }
+    return lo;
+}
+
+__global__ void fill_words_kernel(uint32_t* __restrict__ p, int64_t n, uint32_t v) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+// Largest magnitude pattern per segment.  A workgroup of 4 waves takes
+// kSegRows consecutive rows, a wave one row at a time (16-byte loads across
+// the row); the row maxima are folded by runs of rows of one segment, one
+// atomic max per run.
+constexpr int kSegRows = 32, kSegThreads = 256;
+
+template <int DT>
+__global__ __launch_bounds__(kSegThreads) void seg_amax_kernel(const void* __restrict__ x, int64_t rows,
+                                                               int64_t cols, int64_t ldx,
+                                                               const int32_t* __restrict__ off, int nseg,
+                                                               uint32_t* __restrict__ amax, int vec_in) {
+    __shared__ uint32_t rmax[kSegRows];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int64_t rb = (int64_t)blockIdx.x * kSegRows;
+    constexpr int kPer = DT == FP8_DT_BF16 ? 8 : 4;  // elements per 16 bytes
+    for (int i = w; i < kSegRows; i += kSegThreads / 64) {
+        const int64_t r = rb + i;
+        uint32_t m = 0;
+        if (r < rows) {
+            if (vec_in) {
+                for (int64_t c = (int64_t)lane * kPer; c < cols; c += 64 * kPer) {
+                    const uint4 v = *(const uint4*)((const char*)x + (r * ldx + c) * (DT == FP8_DT_BF16 ? 2 : 4));
+                    if (DT == FP8_DT_BF16) {
+                        us2 mm = fold_bf16(us2{0, 0}, v);
+                        m = max(m, (uint32_t)max(mm.x, mm.y));
+                    } else {
+                        m = fold_f32(m, v);
+                    }
+                }
+            } else {
+                for (int64_t c = lane; c < cols; c += 64) m = max(m, elem_mag<DT>(x, r * ldx + c));
+            }
+        }
+        m = wave_max(m);
+        if (lane == 0) rmax[i] = m;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const int n = (int)min((int64_t)kSegRows, rows - rb);
+        int s = seg_of(off, nseg, rb);
+        uint32_t run = 0;
+        for (int i = 0; i < n; ++i) {
+            const int si = seg_of(off, nseg, rb + i);
+            if (si != s) {
+                atomicMax(amax + s, DT == FP8_DT_BF16 ? run << 16 : run);
+                s = si;
+                run = 0;
+            }
+            run = max(run, rmax[i]);
+        }
+        if (n > 0) atomicMax(amax + s, DT == FP8_DT_BF16 ? run << 16 : run);
+    }
+}
+
+// Eq. 3 per segment, and its bias expanded to every row of the segment.
+template <int FMT>
+__global__ void seg_bias_kernel(const uint32_t* __restrict__ amax, const int32_t* __restrict__ off, int nseg,
+                                int64_t rows, int32_t margin, int32_t* __restrict__ bias,
+                                uint32_t* __restrict__ flags, int32_t* __restrict__ rowb) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < nseg) {
+        uint32_t fl;
+        bias[i] = bias_of<FMT>(amax[i], margin, &fl);
+        if (flags) flags[i] = fl;
+    }
+    if (i < rows) {
+        uint32_t fl;
+        rowb[i] = bias_of<FMT>(amax[seg_of(off, nseg, i)], margin, &fl);
+    }
+}
+
+template <int DT, int FMT>
+__global__ __launch_bounds__(kCastThreads) void cast_rows_kernel(
+    const void* __restrict__ x, int64_t rows, int64_t cols, int64_t ldx, const int32_t* __restrict__ rowb,
+    uint8_t* __restrict__ q, int64_t ldq, uint8_t* __restrict__ qT, int64_t ldqT, int64_t tiles_c, int vec_in,
+    int vec_q, int vec_qT) {
+    __shared__ __attribute__((aligned(16))) uint8_t tile[kCastCols * kCastRows];
+    cast_tile<DT, FMT, false, true>(x, rows, cols, ldx, 0, q, ldq, qT, ldqT, blockIdx.x / tiles_c,
+                                    blockIdx.x % tiles_c, vec_in, vec_q, vec_qT, tile, rowb);
+}
+
+template <int DT, int FMT>
+void launch_quantise_segments_t(const void* x, int64_t rows, int64_t cols, int64_t ldx, int32_t margin,
+                                const int32_t* off, int nseg, int32_t* bias, uint32_t* amax, uint32_t* flags,
+                                int32_t* rowb, uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT, hipStream_t s) {
+    const int esz = DT == FP8_DT_BF16 ? 2 : 4;
+    hipLaunchKernelGGL(fill_words_kernel, dim3((unsigned)std::min<int64_t>(((int64_t)nseg + 255) / 256, 1024)), dim3(256), 0, s,
+                       amax, (int64_t)nseg, 0u);
+    if (rows > 0 && cols > 0) {
+        const int vec_in = ((uintptr_t)x % 16 == 0) && ((ldx * esz) % 16 == 0) && ((cols * esz) % 16 == 0);
+        hipLaunchKernelGGL((seg_amax_kernel<DT>), dim3((unsigned)((rows + kSegRows - 1) / kSegRows)),
+                           dim3(kSegThreads), 0, s, x, rows, cols, ldx, off, nseg, amax, vec_in);
+    }
+    const int64_t nb = (std::max(rows, (int64_t)nseg) + 255) / 256;
+    hipLaunchKernelGGL((seg_bias_kernel<FMT>), dim3((unsigned)nb), dim3(256), 0, s, amax, off, nseg, rows, margin,
+                       bias, flags, rowb);
+    if (rows > 0 && cols > 0 && (q || qT)) {
+        const int64_t tiles_r = (rows + kCastRows - 1) / kCastRows, tiles_c = (cols + kCastCols - 1) / kCastCols;
+        const int vec_in = ((uintptr_t)x % 16 == 0) && ((ldx * esz) % 16 == 0);
+        const int vec_q = q && ((uintptr_t)q % 8 == 0) && (ldq % 8 == 0);
+        const int vec_qT = qT && ((uintptr_t)qT % 16 == 0) && (ldqT % 16 == 0);
+        hipLaunchKernelGGL((cast_rows_kernel<DT, FMT>), dim3((unsigned)(tiles_r * tiles_c)), dim3(kCastThreads), 0, s,
+                           x, rows, cols, ldx, rowb, q, ldq, qT, ldqT, tiles_c, vec_in, vec_q, vec_qT);
+    }
+}
+
+// Statistical mode of n biases (most frequent value; the smallest of equally
+// frequent ones), appended to a ring buffer: ring[*count % capacity] = mode,
+// then *count += 1.  One workgroup; biases outside [-kModeRange, kModeRange)
+// are counted at the nearest end of that range.
+constexpr int kModeRange = 1024;
+
+__global__ __launch_bounds__(256) void bias_mode_kernel(const int32_t* __restrict__ b, int64_t n,
+                                                        int32_t* __restrict__ ring, int64_t capacity,
+                                                        uint32_t* __restrict__ count) {
+    __shared__ uint32_t hist[2 * kModeRange];
+    __shared__ uint64_t best[256];
+    for (int i = threadIdx.x; i < 2 * kModeRange; i += 256) hist[i] = 0;
+    __syncthreads();
+    for (int64_t i = threadIdx.x; i < n; i += 256) {
+        const int v = max(-kModeRange, min(kModeRange - 1, b[i]));
+        atomicAdd(&hist[v + kModeRange], 1u);
+    }
+    __syncthreads();
+    // key: count in the high bits, (2 kModeRange - 1 - bin) in the low 11, so
+    // that the largest key is the most frequent bin, and among equals the lowest
+    uint64_t k = 0;
+    for (int i = threadIdx.x; i < 2 * kModeRange; i += 256)
+        if (hist[i]) k = max(k, ((uint64_t)hist[i] << 11) | (uint64_t)(2 * kModeRange - 1 - i));
+    best[threadIdx.x] = k;
+    __syncthreads();
+    for (int off = 128; off > 0; off >>= 1) {
+        if (threadIdx.x < off) best[threadIdx.x] = max(best[threadIdx.x], best[threadIdx.x + off]);
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        const int bin = 2 * kModeRange - 1 - (int)(best[0] & 0x7FFull);
+        const uint32_t c = *count;
+        ring[c % (uint64_t)capacity] = bin - kModeRange;
+        *count = c + 1;
+    }
+}
+
 }  // namespace
 
 int amax_blocks(int64_t n) {
@@ -459,6 +627,23 @@ int32_t launch_quantise(const void* x, int dt, int64_t rows, int64_t cols, int64
         launch_quantise_t<decltype(D)::value, decltype(F)::value>(x, rows, cols, ldx, margin, bias_pred, bias, amax_bits,
                                                                   flags, q, ldq, qT, ldqT, ws, s);
     });
+    return hip_status();
+}
+
+int32_t launch_quantise_segments(const void* x, int dt, int64_t rows, int64_t cols, int64_t ldx, int fmt,
+                                 int32_t margin, const int32_t* offsets, int nseg, int32_t* bias, uint32_t* amax_bits,
+                                 uint32_t* flags, int32_t* row_bias, uint8_t* q, int64_t ldq, uint8_t* qT,
+                                 int64_t ldqT, hipStream_t s) {
+    with_dt_fmt(dt, fmt, [&](auto D, auto F) {
+        launch_quantise_segments_t<decltype(D)::value, decltype(F)::value>(
+            x, rows, cols, ldx, margin, offsets, nseg, bias, amax_bits, flags, row_bias, q, ldq, qT, ldqT, s);
+    });
+    return hip_status();
+}
+
+int32_t launch_bias_mode(const int32_t* bias, int64_t n, int32_t* ring, int64_t capacity, uint32_t* count,
+                         hipStream_t s) {
+    hipLaunchKernelGGL(bias_mode_kernel, dim3(1), dim3(256), 0, s, bias, n, ring, capacity, count);
     return hip_status();
 }
 

@@ -246,6 +246,46 @@ int32_t fp8_linear_bwd_dx_quantise(const uint8_t* dy8, const int32_t* bg, const 
                                 stream);
 }
 
+int32_t fp8_quantise_segments(const void* x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx, int32_t fmt,
+                              int32_t margin, const int32_t* offsets, int64_t nseg, int32_t* bias,
+                              uint32_t* amax_bits, uint32_t* flags, int32_t* row_bias, uint8_t* q, int64_t ldq,
+                              uint8_t* qT, int64_t ldqT, void* stream) {
+    if (!dt_ok(dt) || !fmt_ok(fmt) || rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return FP8_EINVAL;
+    if (margin < -FP8_MAX_MARGIN || margin > FP8_MAX_MARGIN) return FP8_EINVAL;
+    if (nseg < 1 || nseg > INT32_MAX) return FP8_EINVAL;
+    if (!offsets || !bias || !amax_bits || !aligned(offsets, 4) || !aligned(bias, 4) || !aligned(amax_bits, 4))
+        return FP8_EINVAL;
+    if (flags && !aligned(flags, 4)) return FP8_EINVAL;
+    if (rows > 0 && (!row_bias || !aligned(row_bias, 4))) return FP8_EINVAL;
+    if (rows > 0 && cols > 0) {
+        if (!x || !aligned(x, esize(dt)) || ldx < cols) return FP8_EINVAL;
+        if ((q && ldq < cols) || (qT && ldqT < rows)) return FP8_EINVAL;
+    }
+    return launch_quantise_segments(x, dt, rows, cols, ldx, fmt, margin, offsets, (int)nseg, bias, amax_bits, flags,
+                                    row_bias, q, ldq, qT, ldqT, as_stream(stream));
+}
+
+int32_t fp8_linear_fwd_rows(const uint8_t* x8, const int32_t* bx_rows, const uint8_t* w8t, const int32_t* bw,
+                            void* y, int32_t y_dt, int64_t M, int64_t N, int64_t K, uint32_t* y_amax_bits,
+                            void* stream) {
+    if (!dt_ok(y_dt) || M < 0 || N < 0 || K < 0 || M > kMaxDim || N > kMaxDim || K > kMaxDim) return FP8_EINVAL;
+    if (M == 0 || N == 0) return FP8_OK;
+    if (!y || !bx_rows || !bw || (K > 0 && (!x8 || !w8t))) return FP8_EINVAL;
+    if (!aligned(y, esize(y_dt)) || !aligned(bx_rows, 4) || !aligned(bw, 4)) return FP8_EINVAL;
+    if (y_amax_bits && !aligned(y_amax_bits, 4)) return FP8_EINVAL;
+    if (M > INT32_MAX || N > INT32_MAX) return FP8_ENOTSUP;
+    return launch_gemm_nt(x8, FP8_E4M3, bx_rows, w8t, FP8_E4M3, bw, y, y_dt, M, N, K, y_amax_bits,
+                          as_stream(stream), 1);
+}
+
+int32_t fp8_bias_mode(const int32_t* bias, int64_t n, int32_t* ring, int64_t capacity, uint32_t* count,
+                      void* stream) {
+    if (n < 0 || capacity < 1 || !ring || !count || !aligned(ring, 4) || !aligned(count, 4)) return FP8_EINVAL;
+    if (n == 0) return FP8_OK;
+    if (!bias || !aligned(bias, 4)) return FP8_EINVAL;
+    return launch_bias_mode(bias, n, ring, capacity, count, as_stream(stream));
+}
+
 int32_t ptq_quantise_weights(const void* w, int32_t dt, int64_t K, int64_t N, uint8_t* w8,
                              uint8_t* w8t, int32_t* bw, uint32_t* flags, void* ws, size_t ws_bytes,
                              void* stream) {

@@ -163,6 +163,12 @@ __device__ __forceinline__ uint32_t store4(void* C, int64_t ldc, int64_t m, int6
     return m < M ? mx : 0u;
 }
 
+// Unscale exponent of output row m (of M): -(ba + bb), with ba of row m when
+// ba_rows (per-row activation biases, one per data sample or segment).
+__device__ __forceinline__ int row_shift(const int32_t* ba_p, int ba_rows, int bb, int64_t m, int64_t M) {
+    return -((ba_rows ? ba_p[min(m, M - 1)] : ba_p[0]) + bb);
+}
+
 // ------------------------------------------------------------ main kernel
 constexpr int kBM = 256, kBN = 256, kBK = 128, kThreads = 256;
 constexpr int kMainThreads = 512;      // 8 waves: two groups of four
@@ -247,7 +253,7 @@ template <int FA, int FB, int OUT_DT, bool AMAX, int QF = -1>
 __global__ __launch_bounds__(kMainThreads) void gemm_nt_256(
     const uint8_t* __restrict__ A, const uint8_t* __restrict__ B, const int32_t* __restrict__ ba_p,
     const int32_t* __restrict__ bb_p, void* __restrict__ C, int M, int N, int K, int tiles_m,
-    int tiles_n, int vec_out, uint32_t* __restrict__ amax_out, QuantOut qo, BiasOut bo) {
+    int tiles_n, int vec_out, uint32_t* __restrict__ amax_out, QuantOut qo, BiasOut bo, int ba_rows) {
     static_assert(QF < 0 || OUT_DT == FP8_DT_BF16, "fused quantise is for bf16 outputs");
     __shared__ __attribute__((aligned(1024))) uint8_t smem[kSmemBytes];
 
@@ -370,7 +376,9 @@ __global__ __launch_bounds__(kMainThreads) void gemm_nt_256(
     // The last barrier of the main loop follows every read of the operand
     // tiles, so group 0 stages and stores its outputs while group 1 issues its
     // last MFMAs.
-    const int sh = -(*ba_p + *bb_p);
+    int shr[4];  // unscale exponent of this lane's rows wr0 + 16 i + frow
+#pragma unroll
+    for (int i = 0; i < 4; ++i) shr[i] = row_shift(ba_p, ba_rows, *bb_p, (int64_t)m0 + wr0 + i * 16 + frow, M);
     const int prow = 2 * (lane >> 5) + (((lane >> 2) ^ (lane >> 3) ^ (lane >> 4)) & 1);
     uint32_t mx = 0;
     if (OUT_DT == FP8_DT_BF16) {
@@ -390,8 +398,8 @@ __global__ __launch_bounds__(kMainThreads) void gemm_nt_256(
                 const int i = 2 * i2 + ii;
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
-                    const uint32_t lo = pack_bf16x2(ldexpf(acc[i][j][0], sh), ldexpf(acc[i][j][1], sh));
-                    const uint32_t hi = pack_bf16x2(ldexpf(acc[i][j][2], sh), ldexpf(acc[i][j][3], sh));
+                    const uint32_t lo = pack_bf16x2(ldexpf(acc[i][j][0], shr[i]), ldexpf(acc[i][j][1], shr[i]));
+                    const uint32_t hi = pack_bf16x2(ldexpf(acc[i][j][2], shr[i]), ldexpf(acc[i][j][3], shr[i]));
                     if (AMAX || QF >= 0) {
                         m2 = __builtin_elementwise_max(m2, __builtin_bit_cast(u16x2, lo & 0x7FFF7FFFu));
                         m2 = __builtin_elementwise_max(m2, __builtin_bit_cast(u16x2, hi & 0x7FFF7FFFu));
@@ -489,7 +497,7 @@ __global__ __launch_bounds__(kMainThreads) void gemm_nt_256(
                     float y[4];
 #pragma unroll
                     for (int v = 0; v < 4; ++v) {
-                        y[v] = ldexpf(acc[i][j][v], sh);
+                        y[v] = ldexpf(acc[i][j][v], shr[i]);
                         if (AMAX) mx = max(mx, __float_as_uint(y[v]) & 0x7FFFFFFFu);
                     }
                     *(float4*)(ep + (ii * 16 + frow) * kEpRowF32 + (j * 16 + 4 * fg) * 4) =
@@ -559,7 +567,7 @@ template <int FA, int FB, int OUT_DT, bool AMAX>
 __global__ __launch_bounds__(kThreads) void gemm_nt_small(
     const uint8_t* __restrict__ A, const uint8_t* __restrict__ B, const int32_t* __restrict__ ba_p,
     const int32_t* __restrict__ bb_p, void* __restrict__ C, int64_t M, int64_t N, int64_t K,
-    int64_t tiles_n, int vec_out, uint32_t* __restrict__ amax_out) {
+    int64_t tiles_n, int vec_out, uint32_t* __restrict__ amax_out, int ba_rows) {
     __shared__ __attribute__((aligned(16))) uint8_t sa[kSBM * kBK];
     __shared__ __attribute__((aligned(16))) uint8_t sb[kSBN * kBK];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -615,7 +623,6 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_small(
         __syncthreads();
     }
 
-    const int sh = -(*ba_p + *bb_p);
     uint32_t mx = 0;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
@@ -623,7 +630,7 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_small(
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
             const int64_t n = n0 + wn * 32 + j * 16 + fg * 4;
-            if (n < N) mx = max(mx, store4<OUT_DT>(C, N, m, n, M, N, acc[i][j], sh, vec_out != 0));
+            if (n < N) mx = max(mx, store4<OUT_DT>(C, N, m, n, M, N, acc[i][j], row_shift(ba_p, ba_rows, *bb_p, m, M), vec_out != 0));
         }
     }
     if (AMAX) {
@@ -653,7 +660,7 @@ template <int FA, int FB, int OUT_DT, bool AMAX, int MB, int NB, int kDecWaves>
 __global__ __launch_bounds__(kDecWaves * 64) void gemm_nt_decode(
     const uint8_t* __restrict__ A, const uint8_t* __restrict__ B, const int32_t* __restrict__ ba_p,
     const int32_t* __restrict__ bb_p, void* __restrict__ C, int M, int N, int K, int vec_out,
-    uint32_t* __restrict__ amax_out) {
+    uint32_t* __restrict__ amax_out, int ba_rows) {
     __shared__ __attribute__((aligned(16))) float red[kDecWaves][MB][NB][64][4];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int n0 = blockIdx.x * NB * 16;
@@ -710,7 +717,6 @@ __global__ __launch_bounds__(kDecWaves * 64) void gemm_nt_decode(
 #pragma unroll
         for (int j = 0; j < NB; ++j) *(v4f*)red[w][mb][j][lane] = acc[mb][j];
     __syncthreads();
-    const int sh = -(*ba_p + *bb_p);
     uint32_t mx = 0;
     for (int slot = threadIdx.x; slot < MB * NB * 64; slot += kDecWaves * 64) {
         const int mb = slot / (NB * 64), j = (slot / 64) % NB, l = slot & 63;
@@ -719,7 +725,7 @@ __global__ __launch_bounds__(kDecWaves * 64) void gemm_nt_decode(
         for (int ww = 1; ww < kDecWaves; ++ww) sum += *(const v4f*)red[ww][mb][j][l];
         const int64_t m = mb * 16 + (l & 15);
         const int64_t n = n0 + j * 16 + (l >> 4) * 4;
-        if (n < N) mx = max(mx, store4<OUT_DT>(C, N, m, n, M, N, sum, sh, vec_out != 0));
+        if (n < N) mx = max(mx, store4<OUT_DT>(C, N, m, n, M, N, sum, row_shift(ba_p, ba_rows, *bb_p, m, M), vec_out != 0));
     }
     if (AMAX) {
         mx = wave_max_u32(mx);
@@ -729,13 +735,13 @@ __global__ __launch_bounds__(kDecWaves * 64) void gemm_nt_decode(
 
 template <int FA, int FB, int OUT_DT, bool AMAX, int MB>
 void launch_decode(const uint8_t* A, const int32_t* ba, const uint8_t* B, const int32_t* bb, void* C,
-                   int M, int N, int K, int vec_out, uint32_t* amax, hipStream_t s) {
+                   int M, int N, int K, int vec_out, uint32_t* amax, int ba_rows, hipStream_t s) {
     // 32 output columns per workgroup of 4 waves, each wave a quarter of the
     // K range (the best of 1-8 column blocks x 4-16 waves on the Llama-2-70B
     // decode shapes)
     const int nblk = (N + 31) / 32;
     hipLaunchKernelGGL((gemm_nt_decode<FA, FB, OUT_DT, AMAX, MB, 2, 4>), dim3(nblk), dim3(4 * 64), 0, s, A, B, ba,
-                       bb, C, M, N, K, vec_out, amax);
+                       bb, C, M, N, K, vec_out, amax, ba_rows);
 }
 
 __global__ void fill_u32_kernel(uint32_t* p, uint32_t v) {
@@ -752,22 +758,22 @@ bool fast_path(const uint8_t* A, const uint8_t* B, int64_t M, int64_t N, int64_t
 // bo.ws != nullptr only where the 256 x 256 kernel runs (fast_path, M > 32).
 template <int FA, int FB, int OUT_DT, bool AMAX>
 void launch_t(const uint8_t* A, const int32_t* ba, const uint8_t* B, const int32_t* bb, void* C,
-              int64_t M, int64_t N, int64_t K, uint32_t* amax, const BiasOut& bo, hipStream_t s) {
+              int64_t M, int64_t N, int64_t K, uint32_t* amax, const BiasOut& bo, int ba_rows, hipStream_t s) {
     const int esz = OUT_DT == FP8_DT_BF16 ? 2 : 4;
     const int vec_out = ((uintptr_t)C % (4 * esz) == 0) && (N % 4 == 0);
     const bool fast = fast_path(A, B, M, N, K);
     if (fast && M <= 32) {
-        if (M <= 16) launch_decode<FA, FB, OUT_DT, AMAX, 1>(A, ba, B, bb, C, (int)M, (int)N, (int)K, vec_out, amax, s);
-        else launch_decode<FA, FB, OUT_DT, AMAX, 2>(A, ba, B, bb, C, (int)M, (int)N, (int)K, vec_out, amax, s);
+        if (M <= 16) launch_decode<FA, FB, OUT_DT, AMAX, 1>(A, ba, B, bb, C, (int)M, (int)N, (int)K, vec_out, amax, ba_rows, s);
+        else launch_decode<FA, FB, OUT_DT, AMAX, 2>(A, ba, B, bb, C, (int)M, (int)N, (int)K, vec_out, amax, ba_rows, s);
     } else if (fast) {
         const int tiles_m = (int)((M + kBM - 1) / kBM), tiles_n = (int)((N + kBN - 1) / kBN);
         const int vec16 = ((uintptr_t)C % 16 == 0) && ((N * esz) % 16 == 0);
         hipLaunchKernelGGL((gemm_nt_256<FA, FB, OUT_DT, AMAX>), dim3(tiles_m * tiles_n), dim3(kMainThreads), 0,
-                           s, A, B, ba, bb, C, (int)M, (int)N, (int)K, tiles_m, tiles_n, vec16, amax, QuantOut{}, bo);
+                           s, A, B, ba, bb, C, (int)M, (int)N, (int)K, tiles_m, tiles_n, vec16, amax, QuantOut{}, bo, ba_rows);
     } else {
         const int64_t tiles_m = (M + kSBM - 1) / kSBM, tiles_n = (N + kSBN - 1) / kSBN;
         hipLaunchKernelGGL((gemm_nt_small<FA, FB, OUT_DT, AMAX>), dim3((unsigned)(tiles_m * tiles_n)),
-                           dim3(kThreads), 0, s, A, B, ba, bb, C, M, N, K, tiles_n, vec_out, amax);
+                           dim3(kThreads), 0, s, A, B, ba, bb, C, M, N, K, tiles_n, vec_out, amax, ba_rows);
     }
 }
 
@@ -775,27 +781,27 @@ void launch_t(const uint8_t* A, const int32_t* ba, const uint8_t* B, const int32
 template <int FA, int FB>
 void dispatch_out(const uint8_t* A, const int32_t* ba, const uint8_t* B, const int32_t* bb, void* C,
                   int out_dt, int64_t M, int64_t N, int64_t K, bool with_amax, uint32_t* amax,
-                  const BiasOut& bo, hipStream_t s) {
+                  const BiasOut& bo, int ba_rows, hipStream_t s) {
     if (out_dt == FP8_DT_BF16) {
-        if (with_amax) launch_t<FA, FB, FP8_DT_BF16, true>(A, ba, B, bb, C, M, N, K, amax, bo, s);
-        else launch_t<FA, FB, FP8_DT_BF16, false>(A, ba, B, bb, C, M, N, K, amax, bo, s);
+        if (with_amax) launch_t<FA, FB, FP8_DT_BF16, true>(A, ba, B, bb, C, M, N, K, amax, bo, ba_rows, s);
+        else launch_t<FA, FB, FP8_DT_BF16, false>(A, ba, B, bb, C, M, N, K, amax, bo, ba_rows, s);
     } else {
-        if (with_amax) launch_t<FA, FB, FP8_DT_F32, true>(A, ba, B, bb, C, M, N, K, amax, bo, s);
-        else launch_t<FA, FB, FP8_DT_F32, false>(A, ba, B, bb, C, M, N, K, amax, bo, s);
+        if (with_amax) launch_t<FA, FB, FP8_DT_F32, true>(A, ba, B, bb, C, M, N, K, amax, bo, ba_rows, s);
+        else launch_t<FA, FB, FP8_DT_F32, false>(A, ba, B, bb, C, M, N, K, amax, bo, ba_rows, s);
     }
 }
 
 void dispatch_fmts(const uint8_t* A, int fa, const int32_t* ba, const uint8_t* B, int fb, const int32_t* bb,
                    void* C, int out_dt, int64_t M, int64_t N, int64_t K, bool with_amax, uint32_t* amax,
-                   const BiasOut& bo, hipStream_t s) {
+                   const BiasOut& bo, int ba_rows, hipStream_t s) {
     if (fa == FP8_E4M3 && fb == FP8_E4M3)
-        dispatch_out<FP8_E4M3, FP8_E4M3>(A, ba, B, bb, C, out_dt, M, N, K, with_amax, amax, bo, s);
+        dispatch_out<FP8_E4M3, FP8_E4M3>(A, ba, B, bb, C, out_dt, M, N, K, with_amax, amax, bo, ba_rows, s);
     else if (fa == FP8_E5M2 && fb == FP8_E4M3)
-        dispatch_out<FP8_E5M2, FP8_E4M3>(A, ba, B, bb, C, out_dt, M, N, K, with_amax, amax, bo, s);
+        dispatch_out<FP8_E5M2, FP8_E4M3>(A, ba, B, bb, C, out_dt, M, N, K, with_amax, amax, bo, ba_rows, s);
     else if (fa == FP8_E4M3 && fb == FP8_E5M2)
-        dispatch_out<FP8_E4M3, FP8_E5M2>(A, ba, B, bb, C, out_dt, M, N, K, with_amax, amax, bo, s);
+        dispatch_out<FP8_E4M3, FP8_E5M2>(A, ba, B, bb, C, out_dt, M, N, K, with_amax, amax, bo, ba_rows, s);
     else
-        dispatch_out<FP8_E5M2, FP8_E5M2>(A, ba, B, bb, C, out_dt, M, N, K, with_amax, amax, bo, s);
+        dispatch_out<FP8_E5M2, FP8_E5M2>(A, ba, B, bb, C, out_dt, M, N, K, with_amax, amax, bo, ba_rows, s);
 }
 
 template <int FA, int FB, int QF>
@@ -804,7 +810,7 @@ void launch_fused_t(const uint8_t* A, const int32_t* ba, const uint8_t* B, const
     const int tiles_m = (int)((M + kBM - 1) / kBM), tiles_n = (int)((N + kBN - 1) / kBN);
     const int vec16 = ((uintptr_t)C % 16 == 0) && ((N * 2) % 16 == 0);
     hipLaunchKernelGGL((gemm_nt_256<FA, FB, FP8_DT_BF16, false, QF>), dim3(tiles_m * tiles_n), dim3(kMainThreads), 0,
-                       s, A, B, ba, bb, C, (int)M, (int)N, (int)K, tiles_m, tiles_n, vec16, nullptr, qo, BiasOut{});
+                       s, A, B, ba, bb, C, (int)M, (int)N, (int)K, tiles_m, tiles_n, vec16, nullptr, qo, BiasOut{}, 0);
 }
 
 template <int FA, int FB>
@@ -862,25 +868,26 @@ int32_t launch_gemm_nt_quantise(const uint8_t* A, int fa, const int32_t* ba, con
 
 int32_t launch_gemm_nt(const uint8_t* A, int fa, const int32_t* ba, const uint8_t* B, int fb,
                        const int32_t* bb, void* C, int out_dt, int64_t M, int64_t N, int64_t K,
-                       uint32_t* amax_bits, hipStream_t s) {
+                       uint32_t* amax_bits, hipStream_t s, int ba_rows) {
     if (amax_bits) hipLaunchKernelGGL(fill_u32_kernel, dim3(1), dim3(64), 0, s, amax_bits, 0u);
-    dispatch_fmts(A, fa, ba, B, fb, bb, C, out_dt, M, N, K, amax_bits != nullptr, amax_bits, BiasOut{}, s);
+    dispatch_fmts(A, fa, ba, B, fb, bb, C, out_dt, M, N, K, amax_bits != nullptr, amax_bits, BiasOut{}, ba_rows, s);
     return hip_status();
 }
 
 int32_t launch_gemm_nt_bias(const uint8_t* A, int fa, const int32_t* ba, const uint8_t* B, int fb,
                             const int32_t* bb, void* C, int out_dt, int64_t M, int64_t N, int64_t K, int bfmt,
                             int32_t margin, int32_t* bias, uint32_t* amax_bits, uint32_t* flags, uint32_t* ws,
-                            hipStream_t s) {
+                            hipStream_t s, int ba_rows) {
     if (fast_path(A, B, M, N, K) && M > 32) {
-        dispatch_fmts(A, fa, ba, B, fb, bb, C, out_dt, M, N, K, true, amax_bits, BiasOut{bias, flags, ws, bfmt, margin}, s);
+        dispatch_fmts(A, fa, ba, B, fb, bb, C, out_dt, M, N, K, true, amax_bits, BiasOut{bias, flags, ws, bfmt, margin},
+                      ba_rows, s);
         return hip_status();
     }
     // decode and fallback kernels: amax with atomics into a zeroed word (ws[0]
     // if no amax output is wanted, zeroed again afterwards), then the bias
     uint32_t* acc = amax_bits ? amax_bits : ws;
     hipLaunchKernelGGL(fill_u32_kernel, dim3(1), dim3(64), 0, s, acc, 0u);
-    dispatch_fmts(A, fa, ba, B, fb, bb, C, out_dt, M, N, K, true, acc, BiasOut{}, s);
+    dispatch_fmts(A, fa, ba, B, fb, bb, C, out_dt, M, N, K, true, acc, BiasOut{}, ba_rows, s);
     int32_t st = hip_status();
     if (st != FP8_OK) return st;
     st = launch_bias_from_amax(acc, bfmt, margin, bias, flags, s);

@@ -53,10 +53,23 @@ int32_t launch_gemm_nt_quantise(const uint8_t* A, int fa, const int32_t* ba, con
                                 uint32_t* ws, hipStream_t s);
 
 // C[m, n] = 2^-(*ba + *bb) * sum_k A[m, k] * B[n, k]; A [M, K] (format fa),
-// B [N, K] (format fb), both dense; C [M, N] dense of type out_dt.
+// B [N, K] (format fb), both dense; C [M, N] dense of type out_dt.  With
+// ba_rows, ba holds one bias per row of A: 2^-(ba[m] + *bb).
 int32_t launch_gemm_nt(const uint8_t* A, int fa, const int32_t* ba, const uint8_t* B, int fb,
                        const int32_t* bb, void* C, int out_dt, int64_t M, int64_t N, int64_t K,
-                       uint32_t* amax_bits, hipStream_t s);
+                       uint32_t* amax_bits, hipStream_t s, int ba_rows = 0);
+
+// Per row segment of x (rows offsets[s] .. offsets[s+1]-1): amax, Eq. 3 bias
+// and flags into [nseg] arrays, the bias of every row into row_bias [rows],
+// and the cast of each row with its segment's bias.
+int32_t launch_quantise_segments(const void* x, int dt, int64_t rows, int64_t cols, int64_t ldx, int fmt,
+                                 int32_t margin, const int32_t* offsets, int nseg, int32_t* bias, uint32_t* amax_bits,
+                                 uint32_t* flags, int32_t* row_bias, uint8_t* q, int64_t ldq, uint8_t* qT,
+                                 int64_t ldqT, hipStream_t s);
+
+// Mode of n biases appended to ring[*count % capacity]; *count += 1.
+int32_t launch_bias_mode(const int32_t* bias, int64_t n, int32_t* ring, int64_t capacity, uint32_t* count,
+                         hipStream_t s);
 
 // launch_gemm_nt with the epilogue amax of C turned into the Eq. 3 bias for
 // format bfmt in the same launch (256 x 256 kernel: the last workgroup to
@@ -66,7 +79,7 @@ int32_t launch_gemm_nt(const uint8_t* A, int fa, const int32_t* ba, const uint8_
 int32_t launch_gemm_nt_bias(const uint8_t* A, int fa, const int32_t* ba, const uint8_t* B, int fb,
                             const int32_t* bb, void* C, int out_dt, int64_t M, int64_t N, int64_t K, int bfmt,
                             int32_t margin, int32_t* bias, uint32_t* amax_bits, uint32_t* flags, uint32_t* ws,
-                            hipStream_t s);
+                            hipStream_t s, int ba_rows = 0);
 
 inline int32_t hip_status() { return hipGetLastError() == hipSuccess ? FP8_OK : FP8_EHIP; }
 

@@ -32,6 +32,7 @@ EXPORTS = (
     "fp8_linear_bwd_dx_bias", "fp8_linear_quantise_ws_bytes",
     "fp8_linear_fwd_quantise", "fp8_linear_bwd_dx_quantise",
     "fp8_linear_bwd_dw", "ptq_quantise_weights",
+    "fp8_quantise_segments", "fp8_linear_fwd_rows", "fp8_bias_mode",
 )
 
 
@@ -92,6 +93,13 @@ def lib() -> ctypes.CDLL:
                           i64, vp, sz, vp]
         L.fp8_linear_bwd_dw.restype = i32
         L.fp8_linear_bwd_dw.argtypes = [vp, vp, vp, vp, vp, i32, i64, i64, i64, vp]
+        L.fp8_quantise_segments.restype = i32
+        L.fp8_quantise_segments.argtypes = [vp, i32, i64, i64, i64, i32, i32, vp, i64, vp, vp, vp, vp, vp, i64,
+                                            vp, i64, vp]
+        L.fp8_linear_fwd_rows.restype = i32
+        L.fp8_linear_fwd_rows.argtypes = [vp, vp, vp, vp, vp, i32, i64, i64, i64, vp, vp]
+        L.fp8_bias_mode.restype = i32
+        L.fp8_bias_mode.argtypes = [vp, i64, vp, i64, vp, vp]
         L.ptq_quantise_weights.restype = i32
         L.ptq_quantise_weights.argtypes = [vp, i32, i64, i64, vp, vp, vp, vp, vp, sz, vp]
         _lib = L
@@ -390,3 +398,47 @@ def ptq_quantise_weights(w, want_w8=True, want_w8t=True, w8=None, w8t=None, bw=N
                                     ws.numel() * ws.element_size(), _stream(stream))
     _check("ptq_quantise_weights", st)
     return w8, w8t, bw, flags
+
+
+def fp8_quantise_segments(x: torch.Tensor, offsets: torch.Tensor, fmt: int, margin: int = 0, bias=None,
+                          amax_bits=None, flags=None, row_bias=None, q=None, qT=None, want_q=True,
+                          want_qT=False, stream=None):
+    """amax + Eq. 3 bias + cast per row segment (rows offsets[s] .. offsets[s+1]-1,
+    offsets a device int32 [nseg + 1]).  Returns (q, qT, bias[nseg],
+    amax_bits[nseg], flags[nseg], row_bias[rows])."""
+    rows, cols = x.shape
+    dev = x.device
+    nseg = offsets.numel() - 1
+    i32 = dict(dtype=torch.int32, device=dev)
+    bias = torch.empty(nseg, **i32) if bias is None else bias
+    amax_bits = torch.empty(nseg, **i32) if amax_bits is None else amax_bits
+    flags = torch.empty(nseg, **i32) if flags is None else flags
+    row_bias = torch.empty(max(rows, 1), **i32) if row_bias is None else row_bias
+    if want_q and q is None:
+        q = torch.empty((rows, cols), dtype=torch.uint8, device=dev)
+    if want_qT and qT is None:
+        qT = torch.empty((cols, rows), dtype=torch.uint8, device=dev)
+    st = lib().fp8_quantise_segments(_p(x), _dt(x), rows, cols, _ld(x), fmt, margin, _p(offsets), nseg,
+                                     _p(bias), _p(amax_bits), _p(flags), _p(row_bias), _p(q),
+                                     _ld(q) if q is not None else 0, _p(qT), _ld(qT) if qT is not None else 0,
+                                     _stream(stream))
+    _check("fp8_quantise_segments", st)
+    return q, qT, bias, amax_bits, flags, row_bias[:rows]
+
+
+def fp8_linear_fwd_rows(x8, bx_rows, w8t, bw, out_dt=DT_BF16, y=None, y_amax_bits=None, stream=None):
+    """Y [M,N] = 2^-(bx_rows[m]+bw) X8 [M,K] . W8T [N,K]^T (one activation bias per row)."""
+    M, K = x8.shape
+    N = w8t.shape[0]
+    y = _out((M, N), out_dt, x8.device, y)
+    st = lib().fp8_linear_fwd_rows(_p(x8), _p(bx_rows), _p(w8t), _p(bw), _p(y), _odt(out_dt, y), M, N, K,
+                                   _p(y_amax_bits), _stream(stream))
+    _check("fp8_linear_fwd_rows", st)
+    return y
+
+
+def fp8_bias_mode(bias: torch.Tensor, ring: torch.Tensor, count: torch.Tensor, stream=None):
+    """Append the mode of `bias` to the device ring buffer `ring` at
+    count % capacity and increment `count` (one-element int32), on the device."""
+    st = lib().fp8_bias_mode(_p(bias), bias.numel(), _p(ring), ring.numel(), _p(count), _stream(stream))
+    _check("fp8_bias_mode", st)

@@ -155,3 +155,25 @@ def test_gemm_bias_rejects(L):
         assert f(FAKE, FAKE, FAKE, FAKE, NULL, 0, 4, 4, 4, 0, 0, FAKE, NULL, NULL, FAKE, 8, NULL) == F.EINVAL   # output
         assert f(FAKE, FAKE, FAKE, FAKE, ODD, 0, 4, 4, 4, 0, 0, FAKE, NULL, NULL, FAKE, 8, NULL) == F.EINVAL    # out align
         assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 0, -1, 4, 4, 0, 0, FAKE, NULL, NULL, FAKE, 8, NULL) == F.EINVAL  # M < 0
+
+
+def test_segments_mode_rows_reject(L):
+    f = L.fp8_quantise_segments
+    # (x, dt, rows, cols, ldx, fmt, margin, offsets, nseg, bias, amax, flags, row_bias, q, ldq, qT, ldqT, stream)
+    ok = [FAKE, 0, 4, 8, 8, 0, 0, FAKE, 2, FAKE, FAKE, NULL, FAKE, FAKE, 8, NULL, 0, NULL]
+    for i, bad in ((1, 3), (5, 9), (6, 1 << 20), (8, 0), (7, NULL), (9, NULL), (10, NULL), (12, NULL), (0, NULL),
+                   (0, ODD), (4, 7), (14, 7), (2, -1)):
+        args = list(ok)
+        args[i] = bad
+        assert f(*args) == F.EINVAL, (i, bad)
+    g = L.fp8_linear_fwd_rows
+    assert g(FAKE, NULL, FAKE, FAKE, FAKE, 0, 4, 4, 4, NULL, NULL) == F.EINVAL   # row biases
+    assert g(FAKE, ODD, FAKE, FAKE, FAKE, 0, 4, 4, 4, NULL, NULL) == F.EINVAL    # alignment
+    assert g(FAKE, FAKE, FAKE, FAKE, FAKE, 3, 4, 4, 4, NULL, NULL) == F.EINVAL   # dtype
+    assert g(NULL, NULL, NULL, NULL, NULL, 0, 0, 4, 4, NULL, NULL) == F.OK       # empty
+    h = L.fp8_bias_mode
+    assert h(FAKE, 4, FAKE, 0, FAKE, NULL) == F.EINVAL     # capacity
+    assert h(FAKE, 4, NULL, 3, FAKE, NULL) == F.EINVAL     # ring
+    assert h(FAKE, 4, FAKE, 3, NULL, NULL) == F.EINVAL     # count
+    assert h(NULL, 4, FAKE, 3, FAKE, NULL) == F.EINVAL     # biases
+    assert h(NULL, 0, FAKE, 3, FAKE, NULL) == F.OK         # nothing to count
