@@ -18,6 +18,9 @@ Paper passages (section / equation / table):
     tensor replica (Sec. 4) and per data sample at inference (App. D): each
     row segment is an independent tensor for ``scale_bias`` and ``cast``
   * ``bias_mode``: the statistical mode of per-sample biases (App. D, App. F)
+  * ``oracle.decoder``: the higher-precision glue of the Llama 2 decoder layer
+    (RMSNorm, RoPE, causal grouped-query attention, SwiGLU, residual adds)
+    around its four FP8 linears (App. E), and the layer as a chain (numpy, fp64)
 """
 from __future__ import annotations
 
