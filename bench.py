@@ -29,6 +29,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 FP8_PEAK_TFLOPS = 5000.0     # MI355X dense FP8 MFMA, published
+BF16_PEAK_TFLOPS = 2500.0    # MI355X dense bf16 MFMA, published
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, published
 METRIC = "FP8 linear fwd+bwd TFLOP/s incl. amax+cast, % of FP8 MFMA peak"
 DEFAULT_WORKLOAD = "llama2-7b-up"
@@ -160,7 +161,12 @@ def roofline(step, per_call):
             table[kind] = dict(bound="mfma", achieved=ach, peak=FP8_PEAK_TFLOPS, unit="TFLOP/s",
                                frac=ach / FP8_PEAK_TFLOPS, avg_us=avg * 1e6, per_launch=per_launch,
                                total_ms=k["time"] / steps * 1e3)
-        elif kind in ("amax", "cast", "quantise"):
+        elif kind == "attention":
+            ach = per_launch / avg / 1e12 if avg > 0 else 0.0
+            table[kind] = dict(bound="mfma", achieved=ach, peak=BF16_PEAK_TFLOPS, unit="TFLOP/s",
+                               frac=ach / BF16_PEAK_TFLOPS, avg_us=avg * 1e6, per_launch=per_launch,
+                               total_ms=k["time"] / steps * 1e3)
+        elif kind in ("amax", "cast", "quantise", "glue"):
             ach = per_launch / avg / 1e9 if avg > 0 else 0.0
             table[kind] = dict(bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s",
                                frac=ach / HBM_PEAK_GBS, avg_us=avg * 1e6, per_launch=per_launch,
@@ -252,6 +258,90 @@ def cpu_baseline(w, cpu_tensors, budget_s):
                                                                      t_gemm)}
 
 
+def cpu_baseline_layer(cfg, cpu_tensors, sample_rows=256):
+    """The oracle layer on the first `sample_rows` tokens of the call, with the
+    weights quantised by the oracle beforehand (PTQ, not timed, as on the
+    GPU); extrapolated linearly in tokens (the four linears, >99% of the
+    work, cost the same per token; attention grows faster, so the estimate
+    is optimistic for the oracle)."""
+    import oracle as orc
+    from oracle import decoder as D
+    from paper_2309_17224_amd import workloads as wl
+    bits = {k: wl.bf16_bits(v) for k, v in cpu_tensors.items()}
+    p = {"g_attn": bits["g_attn"][0], "g_mlp": bits["g_mlp"][0]}
+    for name, key in (("qkv", "Wqkv"), ("o", "Wo"), ("gate_up", "Wgu"), ("down", "Wd")):
+        _, w8t, bw, _ = orc.ptq_quantise_weights(bits[key])
+        p[name + "_w8t"], p[name + "_bw"] = w8t, bw
+    n = min(sample_rows, cfg.rows)
+    t0 = time.perf_counter()
+    D.layer_forward(bits["H"][:n], p, min(cfg.seq_len, n), cfg.n_heads, cfg.n_kv_heads, cfg.d_head, cfg.ffn)
+    dt = time.perf_counter() - t0
+    flops = sum(2 * cfg.rows * K * N for _, K, N in cfg.linears())
+    est = dt * cfg.rows / n
+    return {"value": round(flops / est / 1e12, 6), "unit": "TFLOP/s", "cores": orc.num_threads(),
+            "kind": "oracle",
+            "sample": "oracle decoder layer (fp64; numpy matmuls of exactly decoded E4M3 codes) on the first "
+                      "%d of %d tokens, %.1fs, extrapolated linearly in tokens to %.1fs" % (n, cfg.rows, dt, est)}
+
+
+def bench_layer(args, cfg):
+    """One forward call of a Llama 2 decoder layer with its four linears in
+    FP8 (PTQ weights, per-call activation biases fused into the producing
+    kernels).  value = FLOPs of the four linears / layer time."""
+    import torch
+    from paper_2309_17224_amd import decoder as DL
+    from paper_2309_17224_amd import workloads as wl
+    dev = torch.device("cuda:0")
+    t0 = time.time()
+    cpu = {t.name: wl.make_layer_tensor(cfg, t.name) for t in cfg.tensors()}
+    log(f"[bench] generated {len(cpu)} tensors in {time.time() - t0:.1f}s")
+    W = {k: v.to(dev) for k, v in cpu.items() if k != "H"}
+    layer = DL.DecoderLayer(cfg, W, dev)
+    layer.H.copy_(cpu["H"].to(dev))
+    del W
+    torch.cuda.synchronize()
+    log(f"[bench] {cfg.name}: {len(layer.calls)} calls per layer; warmup {args.warmup}, steps {args.steps}")
+    wall, per_call, _ = time_steps(layer, args.steps, args.warmup)
+    eager_s = wall / args.steps
+    step_s = eager_s
+    if args.launch == "graph":
+        gwall, _ = time_graph(layer, args.steps, args.warmup)
+        step_s = gwall / args.steps
+    flops = layer.linear_flops()
+    value = flops / step_s / 1e12
+    roof, table = roofline(layer, per_call)
+    for kind, d in sorted(table.items()):
+        log(f"[bench] {kind:9s} " + " ".join(f"{k}={v:.4g}" if isinstance(v, float) else f"{k}={v}"
+                                             for k, v in d.items()))
+    for i, (label, kind, work, _) in enumerate(layer.calls):
+        avg = sum(pc[i] for pc in per_call) / len(per_call)
+        log(f"[bench]   {label:32s} {avg * 1e6:8.1f} us")
+    out = {
+        "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_s * 1e3, 4),
+        "eager_ms_per_step": round(eager_s * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "fp8",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "description": cfg.description,
+                   "linears": [dict(name=n, M=cfg.rows, K=K, N=N) for n, K, N in cfg.linears()],
+                   "mode": "PTQ inference, one decoder layer fwd (four FP8 linears; RMSNorm, RoPE, "
+                           "attention, SwiGLU in bf16 with fused FP8-AMAX quantise)",
+                   "accumulate": "fp32", "outputs": "bf16",
+                   "launch": ("one HIP graph replay per layer call" if args.launch == "graph"
+                              else "one host call per library call")},
+        "frac_of_fp8_peak": round(value / FP8_PEAK_TFLOPS, 4),
+        "roofline": roof,
+        "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv) for kk, vv in d.items()}
+                    for k, d in table.items()},
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline_layer(cfg, cpu)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -274,6 +364,9 @@ def main():
         print(json.dumps({"copy_bytes_per_launch": nbytes, "launches": args.steps}))
         return
     fp8lin.lib()  # fails loudly when the HIP library is missing
+    if args.workload in wl.LAYERS:
+        bench_layer(args, wl.LAYERS[args.workload])
+        return
     w = wl.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
     cpu = make_inputs(w)

@@ -19,7 +19,7 @@
  * E5M2, which are the "(b)" rows of Table 7 (App. A): E4M3 bias 7, max 448,
  * NaN = S.1111.111, no infinity; E5M2 bias 15, max 57344, IEEE infinities
  * and NaNs.  The paper's default "(a)" formats (bias 8 / 16, NaN = 0x80) are
- * not produced by this library.
+ * accepted by the bias and cast calls only (FP8_E4_A, FP8_E5_A below).
  *
  * Conventions shared by every call
  * --------------------------------
@@ -339,6 +339,102 @@ int32_t fp8_linear_bwd_dw(const uint8_t *x8t, const int32_t *bx, const uint8_t *
 int32_t ptq_quantise_weights(const void *w, int32_t dt, int64_t K, int64_t N, uint8_t *w8,
                              uint8_t *w8t, int32_t *bw, uint32_t *flags, void *ws,
                              size_t ws_bytes, void *stream);
+
+/*
+ * ---- Llama 2 decoder layer: the higher-precision layers (App. E) ---------
+ * The paper quantises the four linear layers of each decoder layer to FP8
+ * (QKV projection, attention output projection, the two feed-forward
+ * layers) and keeps the rest in higher precision; the Llama 2 decoder has
+ * RMSNorm pre-normalisation, SwiGLU, rotary position embeddings and, in the
+ * 70B model, grouped-query attention (Sec. 4.3, Table 1).  These calls are
+ * that rest, in bf16 with fp32 arithmetic; every output is rounded once to
+ * bf16 (nearest even).  All tensors are bf16, row-major, 16-byte aligned,
+ * with row strides (ld*, in elements) that are multiples of 8.
+ *
+ * Fused quantise.  Where an FP8 linear consumes the output (RMSNorm, attention,
+ * SwiGLU), the call can also produce its FP8-AMAX codes (Sec. 2.3 Eq. 3,
+ * Sec. 2.1 Eq. 1): pass q (codes [rows, cols], 8-byte aligned, row stride ldq
+ * a multiple of 8) and the arguments of fp8_quantise (fmt, margin,
+ * bias_pred, bias, amax_bits, flags) with a workspace of the op's *_ws_bytes.
+ * The bf16 output, bias, amax, flags and codes are bit for bit those of the
+ * op followed by fp8_quantise of its output: the kernel casts with the
+ * prediction while it takes the amax, and only a wrong prediction costs a
+ * re-cast from the bf16 output.  q == NULL: no quantise (fmt, margin,
+ * bias_pred, bias, amax_bits, flags and ws are then ignored).  An empty
+ * output with q gives amax 0, bias 0 and FP8_FLAG_ZERO.
+ * The workspace is scratch; concurrent calls need distinct workspaces.
+ * Outputs must not overlap inputs unless stated.
+ */
+
+/*
+ * llama_rmsnorm_quantise -- RMSNorm of each row, optionally of a residual sum:
+ *   h = x (res == NULL) or round(x + res);
+ *   y = round(h / sqrt(mean_j h_j^2 + eps) * g)
+ * x, res: [rows, cols] (row strides ldx, ldr); g: the gain [cols].
+ * h: out, optional, [rows, cols] (the new residual stream).
+ * y: out, [rows, cols].  cols a multiple of 8; eps >= 0 (Llama 2: 1e-5).
+ * The mean square is accumulated in fp32 in a fixed order.
+ */
+size_t llama_rmsnorm_ws_bytes(int64_t rows);
+int32_t llama_rmsnorm_quantise(const void *x, int64_t ldx, const void *res, int64_t ldr, const void *g,
+                               int64_t rows, int64_t cols, float eps, void *h, int64_t ldh, void *y,
+                               int64_t ldy, int32_t fmt, int32_t margin, const int32_t *bias_pred,
+                               int32_t *bias, uint32_t *amax_bits, uint32_t *flags, uint8_t *q, int64_t ldq,
+                               void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * llama_rope_table -- (cos, sin) of pos * theta^(-2i/d_head) for positions
+ * 0 .. seq_len-1 and i < d_head/2, evaluated in fp64 and rounded to fp32:
+ * table[2 * (pos * d_head/2 + i) + {0, 1}] (device, 8-byte aligned,
+ * seq_len * d_head floats).  d_head a multiple of 16; theta > 0 (Llama 2: 10000).
+ *
+ * llama_rope -- rotary embedding, in place, of n_heads consecutive heads of
+ * d_head columns starting at x: element i < d_head/2 of a head pairs with
+ * element i + d_head/2 ("rotate half"), row r sits at position r mod seq_len:
+ *   (a, b) -> round(a cos - b sin), round(b cos + a sin).
+ * x: [rows, ld] with ld >= n_heads * d_head; table from llama_rope_table with
+ * the same seq_len and d_head.
+ */
+int32_t llama_rope_table(int64_t seq_len, int32_t d_head, double theta, float *table, void *stream);
+int32_t llama_rope(void *x, int64_t rows, int64_t ld, int32_t n_heads, int32_t d_head, int64_t seq_len,
+                   const float *table, void *stream);
+
+/*
+ * llama_attention -- causal softmax attention with grouped-query heads:
+ *   o_i = sum_{j <= i} softmax_j(q_i . k_j / sqrt(d_head)) v_j
+ * within each sequence of seq_len consecutive rows (the last may be shorter).
+ * qkv: [rows, ld], the QKV projection's output (after llama_rope on the Q and
+ *      K heads): n_heads query heads, then n_kv_heads key heads, then
+ *      n_kv_heads value heads, d_head columns each; query head h reads
+ *      key/value head h / (n_heads / n_kv_heads).
+ * o:   out, [rows, n_heads * d_head], row stride ldo.
+ * d_head must be 128 (FP8_ENOTSUP otherwise); n_kv_heads divides n_heads.
+ * Softmax in fp32; the probabilities are rounded to bf16 for the product
+ * with V (accumulated in fp32).
+ */
+size_t llama_attention_ws_bytes(int64_t rows, int64_t seq_len, int32_t n_heads);
+int32_t llama_attention(const void *qkv, int64_t rows, int64_t ld, int64_t seq_len, int32_t n_heads,
+                        int32_t n_kv_heads, int32_t d_head, void *o, int64_t ldo, int32_t fmt, int32_t margin,
+                        const int32_t *bias_pred, int32_t *bias, uint32_t *amax_bits, uint32_t *flags,
+                        uint8_t *q, int64_t ldq, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * llama_swiglu_quantise -- SwiGLU on the fused gate+up projection output:
+ *   a = round(g * sigmoid(g) * u),  g = gu[:, 0 .. ffn), u = gu[:, ffn .. 2 ffn)
+ * gu: [rows, ldgu >= 2 ffn]; a: out, [rows, ffn] (row stride lda).
+ * ffn a multiple of 8.
+ */
+size_t llama_swiglu_ws_bytes(void);
+int32_t llama_swiglu_quantise(const void *gu, int64_t ldgu, int64_t rows, int64_t ffn, void *a, int64_t lda,
+                              int32_t fmt, int32_t margin, const int32_t *bias_pred, int32_t *bias,
+                              uint32_t *amax_bits, uint32_t *flags, uint8_t *q, int64_t ldq, void *ws,
+                              size_t ws_bytes, void *stream);
+
+/*
+ * llama_residual_add -- out = round(a + b) over n elements (dense, n a
+ * multiple of 8); out may be a or b.  Exact rounding of the sum.
+ */
+int32_t llama_residual_add(const void *a, const void *b, void *out, int64_t n, void *stream);
 
 #ifdef __cplusplus
 }

@@ -102,27 +102,30 @@ def rope(x: np.ndarray, seq_len: int, d_head: int, theta: float = ROPE_THETA) ->
 
 
 def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, seq_len: int, n_heads: int,
-              n_kv_heads: int, d_head: int, rows: np.ndarray | None = None) -> np.ndarray:
-    """Causal softmax attention, per sequence of seq_len consecutive rows:
-    o_i = sum_{j <= i} softmax_j(q_i . k_j / sqrt(d_head)) v_j for each query
-    head; query head h uses key/value head h // (n_heads / n_kv_heads).
-    q [R, n_heads*d_head], k and v [R, n_kv_heads*d_head], bf16 bits.  If rows
-    is given only those query rows are computed.  Returns bf16 bits."""
+              n_kv_heads: int, d_head: int) -> np.ndarray:
+    """Causal softmax attention, per sequence of seq_len consecutive rows
+    (the last may be shorter): o_i = sum_{j <= i} softmax_j(q_i . k_j /
+    sqrt(d_head)) v_j for each query head; query head h uses key/value head
+    h // (n_heads / n_kv_heads).  q [R, n_heads*d_head], k and v
+    [R, n_kv_heads*d_head], bf16 bits.  Per sequence and head, the scores are
+    one fp64 matrix product, masked above the diagonal; the softmax weights
+    are exp(s - max_j s) and the weighted sum of values is divided by their
+    sum.  Returns bf16 bits."""
     R = q.shape[0]
     group = n_heads // n_kv_heads
     qv, kv, vv = bf16_to_f64(q), bf16_to_f64(k), bf16_to_f64(v)
-    sel = np.arange(R) if rows is None else np.asarray(rows, dtype=np.int64)
-    out = np.zeros((sel.size, n_heads * d_head))
-    for t, i in enumerate(sel):
-        start = (i // seq_len) * seq_len            # first row of i's sequence
+    out = np.zeros((R, n_heads * d_head))
+    for s0 in range(0, R, seq_len):
+        s1 = min(s0 + seq_len, R)
+        causal = np.tril(np.ones((s1 - s0, s1 - s0), dtype=bool))
         for h in range(n_heads):
             hk = h // group
-            qi = qv[i, h * d_head:(h + 1) * d_head]
-            K = kv[start:i + 1, hk * d_head:(hk + 1) * d_head]
-            V = vv[start:i + 1, hk * d_head:(hk + 1) * d_head]
-            s = K @ qi / np.sqrt(d_head)
-            p = np.exp(s - s.max())
-            out[t, h * d_head:(h + 1) * d_head] = (p @ V) / p.sum()
+            Q = qv[s0:s1, h * d_head:(h + 1) * d_head]
+            K = kv[s0:s1, hk * d_head:(hk + 1) * d_head]
+            V = vv[s0:s1, hk * d_head:(hk + 1) * d_head]
+            sc = np.where(causal, Q @ K.T / np.sqrt(d_head), -np.inf)
+            p = np.exp(sc - sc.max(axis=1, keepdims=True))
+            out[s0:s1, h * d_head:(h + 1) * d_head] = (p @ V) / p.sum(axis=1, keepdims=True)
     return round_bf16(out)
 
 

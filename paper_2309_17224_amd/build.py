@@ -14,7 +14,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libfp8lin.so")
-SOURCES = ["fp8lin_api.hip", "fp8lin_amax_cast.hip", "fp8lin_gemm.hip"]
+SOURCES = ["fp8lin_api.hip", "fp8lin_amax_cast.hip", "fp8lin_gemm.hip", "fp8lin_decoder.hip"]
 ARCH = "gfx950"
 
 

@@ -14,6 +14,7 @@ bool dt_ok(int32_t d) { return d == FP8_DT_BF16 || d == FP8_DT_F32; }
 int esize(int32_t d) { return d == FP8_DT_BF16 ? 2 : 4; }
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 hipStream_t as_stream(void* s) { return (hipStream_t)s; }
+bool a16(const void* p) { return aligned(p, 16); }
 
 int32_t cast_common(const void* x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx,
                     const int32_t* bias, uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT,
@@ -37,6 +38,46 @@ int32_t gemm_common(const uint8_t* a, int fa, const int32_t* ba, const uint8_t* 
     if (amax && !aligned(amax, 4)) return FP8_EINVAL;
     if (M > INT32_MAX || N > INT32_MAX) return FP8_ENOTSUP;
     return launch_gemm_nt(a, fa, ba, b, fb, bb, c, c_dt, M, N, K, amax, as_stream(stream));
+}
+
+
+// ---- decoder-layer glue: shared checks
+bool rows_ok(int64_t ld, int64_t cols) { return ld >= cols && ld % 8 == 0; }
+
+// Checks the arguments of a fused quantise and fills *fq; q == NULL means no
+// quantise (the other arguments are then ignored).  need_words: workspace
+// words the op needs.
+int32_t glue_quant(int32_t fmt, int32_t margin, const int32_t* pred, int32_t* bias, uint32_t* amax_bits,
+                   uint32_t* flags, uint8_t* q, int64_t ldq, int64_t cols, void* ws, size_t ws_bytes,
+                   int64_t need_words, FusedQuant* fq) {
+    fq->q = nullptr;
+    if (!q) return FP8_OK;
+    if (!fmt_ok(fmt) || margin < -FP8_MAX_MARGIN || margin > FP8_MAX_MARGIN) return FP8_EINVAL;
+    if (!bias || !aligned(bias, 4) || (pred && !aligned(pred, 4))) return FP8_EINVAL;
+    if ((amax_bits && !aligned(amax_bits, 4)) || (flags && !aligned(flags, 4))) return FP8_EINVAL;
+    if (!aligned(q, 8) || !rows_ok(ldq, cols)) return FP8_EINVAL;
+    if (!ws || !aligned(ws, 4) || ws_bytes < (size_t)need_words * sizeof(uint32_t)) return FP8_EINVAL;
+    if (need_words - 1 > INT32_MAX) return FP8_ENOTSUP;
+    fq->fmt = fmt;
+    fq->margin = margin;
+    fq->pred = pred;
+    fq->bias = bias;
+    fq->amax_bits = amax_bits;
+    fq->flags = flags;
+    fq->q = q;
+    fq->ldq = ldq;
+    fq->ws = (uint32_t*)ws;
+    return FP8_OK;
+}
+
+// An empty output with a quantise: amax 0, bias 0 and the zero flag.
+int32_t glue_empty(int32_t fmt, int32_t margin, int32_t* bias, uint32_t* amax_bits, uint32_t* flags, uint8_t* q,
+                   void* stream) {
+    if (!q) return FP8_OK;
+    if (!fmt_ok(fmt) || margin < -FP8_MAX_MARGIN || margin > FP8_MAX_MARGIN || !bias || !aligned(bias, 4))
+        return FP8_EINVAL;
+    if ((amax_bits && !aligned(amax_bits, 4)) || (flags && !aligned(flags, 4))) return FP8_EINVAL;
+    return launch_scale_bias(nullptr, FP8_DT_BF16, 0, fmt, margin, bias, amax_bits, flags, nullptr, as_stream(stream));
 }
 
 }  // namespace
@@ -294,6 +335,96 @@ int32_t ptq_quantise_weights(const void* w, int32_t dt, int64_t K, int64_t N, ui
     int32_t st = fp8_scale_bias(w, dt, K * N, FP8_E4M3, 0, bw, nullptr, flags, ws, ws_bytes, stream);
     if (st != FP8_OK || K == 0 || N == 0) return st;
     return cast_common(w, dt, K, N, N, bw, w8, N, w8t, K, FP8_E4M3, stream);
+}
+
+// ---- decoder-layer glue (App. E)
+size_t llama_rmsnorm_ws_bytes(int64_t rows) {
+    if (rows <= 0 || rows > kMaxDim) return 0;
+    return (size_t)(1 + glue_parts_rmsnorm(rows)) * sizeof(uint32_t);
+}
+
+int32_t llama_rmsnorm_quantise(const void* x, int64_t ldx, const void* res, int64_t ldr, const void* g, int64_t rows,
+                               int64_t cols, float eps, void* h, int64_t ldh, void* y, int64_t ldy, int32_t fmt,
+                               int32_t margin, const int32_t* bias_pred, int32_t* bias, uint32_t* amax_bits,
+                               uint32_t* flags, uint8_t* q, int64_t ldq, void* ws, size_t ws_bytes, void* stream) {
+    if (rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return FP8_EINVAL;
+    if (!(eps >= 0.0f) || eps > 3.0e38f) return FP8_EINVAL;
+    FusedQuant fq;
+    if (rows == 0 || cols == 0) return glue_empty(fmt, margin, bias, amax_bits, flags, q, stream);
+    if (!x || !g || !y || !a16(x) || !a16(g) || !a16(y) || cols % 8) return FP8_EINVAL;
+    if (!rows_ok(ldx, cols) || !rows_ok(ldy, cols)) return FP8_EINVAL;
+    if (res && (!a16(res) || !rows_ok(ldr, cols))) return FP8_EINVAL;
+    if (h && (!a16(h) || !rows_ok(ldh, cols))) return FP8_EINVAL;
+    if (rows > INT32_MAX) return FP8_ENOTSUP;
+    const int32_t st = glue_quant(fmt, margin, bias_pred, bias, amax_bits, flags, q, ldq, cols, ws, ws_bytes,
+                                  1 + glue_parts_rmsnorm(rows), &fq);
+    if (st != FP8_OK) return st;
+    return launch_rmsnorm((const uint16_t*)x, ldx, (const uint16_t*)res, ldr, (const uint16_t*)g, rows, cols, eps,
+                          (uint16_t*)h, ldh, (uint16_t*)y, ldy, &fq, as_stream(stream));
+}
+
+int32_t llama_rope_table(int64_t seq_len, int32_t d_head, double theta, float* table, void* stream) {
+    if (seq_len < 1 || seq_len > kMaxDim || d_head < 16 || d_head % 16 || d_head > 4096) return FP8_EINVAL;
+    if (!(theta > 0.0) || theta > 1e300 || !table || !aligned(table, 8)) return FP8_EINVAL;
+    return launch_rope_table(seq_len, d_head, theta, table, as_stream(stream));
+}
+
+int32_t llama_rope(void* x, int64_t rows, int64_t ld, int32_t n_heads, int32_t d_head, int64_t seq_len,
+                   const float* table, void* stream) {
+    if (rows < 0 || rows > kMaxDim || n_heads < 0 || seq_len < 1 || seq_len > kMaxDim) return FP8_EINVAL;
+    if (d_head < 16 || d_head % 16 || d_head > 4096) return FP8_EINVAL;
+    if (rows == 0 || n_heads == 0) return FP8_OK;
+    if (!x || !a16(x) || !rows_ok(ld, (int64_t)n_heads * d_head) || !table || !aligned(table, 8)) return FP8_EINVAL;
+    return launch_rope((uint16_t*)x, rows, ld, n_heads, d_head, seq_len, table, as_stream(stream));
+}
+
+size_t llama_attention_ws_bytes(int64_t rows, int64_t seq_len, int32_t n_heads) {
+    if (rows <= 0 || seq_len < 1 || n_heads < 1 || rows > kMaxDim || seq_len > kMaxDim) return 0;
+    return (size_t)(1 + glue_parts_attention(rows, seq_len, n_heads)) * sizeof(uint32_t);
+}
+
+int32_t llama_attention(const void* qkv, int64_t rows, int64_t ld, int64_t seq_len, int32_t n_heads,
+                        int32_t n_kv_heads, int32_t d_head, void* o, int64_t ldo, int32_t fmt, int32_t margin,
+                        const int32_t* bias_pred, int32_t* bias, uint32_t* amax_bits, uint32_t* flags, uint8_t* q,
+                        int64_t ldq, void* ws, size_t ws_bytes, void* stream) {
+    if (rows < 0 || rows > kMaxDim || seq_len < 1 || seq_len > kMaxDim) return FP8_EINVAL;
+    if (n_heads < 1 || n_kv_heads < 1 || n_heads % n_kv_heads) return FP8_EINVAL;
+    if (d_head != 128) return FP8_ENOTSUP;
+    FusedQuant fq;
+    if (rows == 0) return glue_empty(fmt, margin, bias, amax_bits, flags, q, stream);
+    const int64_t cols = (int64_t)n_heads * d_head;
+    if (!qkv || !o || !a16(qkv) || !a16(o)) return FP8_EINVAL;
+    if (!rows_ok(ld, (int64_t)(n_heads + 2 * n_kv_heads) * d_head) || !rows_ok(ldo, cols)) return FP8_EINVAL;
+    if (glue_parts_attention(rows, seq_len, n_heads) > INT32_MAX) return FP8_ENOTSUP;
+    const int32_t st = glue_quant(fmt, margin, bias_pred, bias, amax_bits, flags, q, ldq, cols, ws, ws_bytes,
+                                  1 + glue_parts_attention(rows, seq_len, n_heads), &fq);
+    if (st != FP8_OK) return st;
+    return launch_attention((const uint16_t*)qkv, rows, ld, seq_len, n_heads, n_kv_heads, (uint16_t*)o, ldo, &fq,
+                            as_stream(stream));
+}
+
+size_t llama_swiglu_ws_bytes(void) { return (size_t)(1 + glue_parts_swiglu()) * sizeof(uint32_t); }
+
+int32_t llama_swiglu_quantise(const void* gu, int64_t ldgu, int64_t rows, int64_t ffn, void* a, int64_t lda,
+                              int32_t fmt, int32_t margin, const int32_t* bias_pred, int32_t* bias,
+                              uint32_t* amax_bits, uint32_t* flags, uint8_t* q, int64_t ldq, void* ws,
+                              size_t ws_bytes, void* stream) {
+    if (rows < 0 || ffn < 0 || rows > kMaxDim || ffn > kMaxDim) return FP8_EINVAL;
+    FusedQuant fq;
+    if (rows == 0 || ffn == 0) return glue_empty(fmt, margin, bias, amax_bits, flags, q, stream);
+    if (!gu || !a || !a16(gu) || !a16(a) || ffn % 8) return FP8_EINVAL;
+    if (!rows_ok(ldgu, 2 * ffn) || !rows_ok(lda, ffn)) return FP8_EINVAL;
+    const int32_t st = glue_quant(fmt, margin, bias_pred, bias, amax_bits, flags, q, ldq, ffn, ws, ws_bytes,
+                                  1 + glue_parts_swiglu(), &fq);
+    if (st != FP8_OK) return st;
+    return launch_swiglu((const uint16_t*)gu, ldgu, rows, ffn, (uint16_t*)a, lda, &fq, as_stream(stream));
+}
+
+int32_t llama_residual_add(const void* a, const void* b, void* out, int64_t n, void* stream) {
+    if (n < 0 || n > kMaxDim * 64 || n % 8) return FP8_EINVAL;
+    if (n == 0) return FP8_OK;
+    if (!a || !b || !out || !a16(a) || !a16(b) || !a16(out)) return FP8_EINVAL;
+    return launch_residual_add((const uint16_t*)a, (const uint16_t*)b, (uint16_t*)out, n, as_stream(stream));
 }
 
 }  // extern "C"

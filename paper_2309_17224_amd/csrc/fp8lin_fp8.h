@@ -244,6 +244,13 @@ __device__ __forceinline__ uint4 ld_stream(const void* p) {
     return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// Two fp32 -> two bf16 (round to nearest even, v_cvt_pk_bf16_f32) in one word.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
+}
+
 // Biases beyond this saturate or flush every input; casts clamp to it.
 __device__ __forceinline__ int clamp_bias(int32_t b) { return max(-kBiasClamp, min(kBiasClamp, b)); }
 

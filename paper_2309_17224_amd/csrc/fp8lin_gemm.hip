@@ -188,13 +188,6 @@ __device__ __forceinline__ void lds_dma16_s(const uint8_t* sbase, uint32_t voff,
                  : "memory");
 }
 
-// Two fp32 -> two bf16 (round to nearest even, v_cvt_pk_bf16_f32) in one word.
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
-}
-
 __device__ __forceinline__ int bq_used(const int32_t* pred) { return clamp_bias(*pred); }
 
 // 16-byte store of matmul output with the non-temporal hint: the output is not

@@ -81,6 +81,38 @@ int32_t launch_gemm_nt_bias(const uint8_t* A, int fa, const int32_t* ba, const u
                             int32_t margin, int32_t* bias, uint32_t* amax_bits, uint32_t* flags, uint32_t* ws,
                             hipStream_t s, int ba_rows = 0);
 
+// ---- decoder-layer glue (fp8lin_decoder.hip)
+// The FP8-AMAX quantise fused into a glue kernel's bf16 output: codes cast
+// with the prediction (if any), then the exact-bias check and recast.
+struct FusedQuant {
+    int fmt;
+    int32_t margin;
+    const int32_t* pred;  // predicted bias (device) or null
+    int32_t* bias;
+    uint32_t* amax_bits;  // may be null
+    uint32_t* flags;      // may be null
+    uint8_t* q;           // codes [rows, cols], row stride ldq; null: no quantise
+    int64_t ldq;
+    uint32_t* ws;         // word 0: the bias the codes were cast with; then one maximum per workgroup
+};
+
+// Workgroup maxima each glue kernel writes (workspace words beyond the first).
+int64_t glue_parts_rmsnorm(int64_t rows);
+int64_t glue_parts_swiglu();
+int64_t glue_parts_attention(int64_t rows, int64_t seq_len, int nh);
+
+int32_t launch_residual_add(const uint16_t* a, const uint16_t* b, uint16_t* out, int64_t n, hipStream_t s);
+int32_t launch_rmsnorm(const uint16_t* x, int64_t ldx, const uint16_t* res, int64_t ldr, const uint16_t* g,
+                       int64_t rows, int64_t cols, float eps, uint16_t* h, int64_t ldh, uint16_t* y, int64_t ldy,
+                       const FusedQuant* fq, hipStream_t s);
+int32_t launch_rope_table(int64_t seq_len, int d_head, double theta, float* table, hipStream_t s);
+int32_t launch_rope(uint16_t* x, int64_t rows, int64_t ld, int nheads, int d_head, int64_t seq_len,
+                    const float* table, hipStream_t s);
+int32_t launch_swiglu(const uint16_t* gu, int64_t ldgu, int64_t rows, int64_t ffn, uint16_t* a, int64_t lda,
+                      const FusedQuant* fq, hipStream_t s);
+int32_t launch_attention(const uint16_t* qkv, int64_t rows, int64_t ld, int64_t seq_len, int nh, int nkv,
+                         uint16_t* o, int64_t ldo, const FusedQuant* fq, hipStream_t s);
+
 inline int32_t hip_status() { return hipGetLastError() == hipSuccess ? FP8_OK : FP8_EHIP; }
 
 }  // namespace fp8lin

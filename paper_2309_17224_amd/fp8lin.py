@@ -33,6 +33,9 @@ EXPORTS = (
     "fp8_linear_fwd_quantise", "fp8_linear_bwd_dx_quantise",
     "fp8_linear_bwd_dw", "ptq_quantise_weights",
     "fp8_quantise_segments", "fp8_linear_fwd_rows", "fp8_bias_mode",
+    "llama_rmsnorm_ws_bytes", "llama_rmsnorm_quantise", "llama_rope_table", "llama_rope",
+    "llama_attention_ws_bytes", "llama_attention", "llama_swiglu_ws_bytes", "llama_swiglu_quantise",
+    "llama_residual_add",
 )
 
 
@@ -100,6 +103,28 @@ def lib() -> ctypes.CDLL:
         L.fp8_linear_fwd_rows.argtypes = [vp, vp, vp, vp, vp, i32, i64, i64, i64, vp, vp]
         L.fp8_bias_mode.restype = i32
         L.fp8_bias_mode.argtypes = [vp, i64, vp, i64, vp, vp]
+        f32, f64 = ctypes.c_float, ctypes.c_double
+        L.llama_rmsnorm_ws_bytes.restype = sz
+        L.llama_rmsnorm_ws_bytes.argtypes = [i64]
+        L.llama_rmsnorm_quantise.restype = i32
+        L.llama_rmsnorm_quantise.argtypes = [vp, i64, vp, i64, vp, i64, i64, f32, vp, i64, vp, i64, i32, i32,
+                                             vp, vp, vp, vp, vp, i64, vp, sz, vp]
+        L.llama_rope_table.restype = i32
+        L.llama_rope_table.argtypes = [i64, i32, f64, vp, vp]
+        L.llama_rope.restype = i32
+        L.llama_rope.argtypes = [vp, i64, i64, i32, i32, i64, vp, vp]
+        L.llama_attention_ws_bytes.restype = sz
+        L.llama_attention_ws_bytes.argtypes = [i64, i64, i32]
+        L.llama_attention.restype = i32
+        L.llama_attention.argtypes = [vp, i64, i64, i64, i32, i32, i32, vp, i64, i32, i32, vp, vp, vp, vp, vp,
+                                      i64, vp, sz, vp]
+        L.llama_swiglu_ws_bytes.restype = sz
+        L.llama_swiglu_ws_bytes.argtypes = []
+        L.llama_swiglu_quantise.restype = i32
+        L.llama_swiglu_quantise.argtypes = [vp, i64, i64, i64, vp, i64, i32, i32, vp, vp, vp, vp, vp, i64, vp,
+                                            sz, vp]
+        L.llama_residual_add.restype = i32
+        L.llama_residual_add.argtypes = [vp, vp, vp, i64, vp]
         L.ptq_quantise_weights.restype = i32
         L.ptq_quantise_weights.argtypes = [vp, i32, i64, i64, vp, vp, vp, vp, vp, sz, vp]
         _lib = L
@@ -442,3 +467,103 @@ def fp8_bias_mode(bias: torch.Tensor, ring: torch.Tensor, count: torch.Tensor, s
     count % capacity and increment `count` (one-element int32), on the device."""
     st = lib().fp8_bias_mode(_p(bias), bias.numel(), _p(ring), ring.numel(), _p(count), _stream(stream))
     _check("fp8_bias_mode", st)
+
+
+# ------------------------------------------------------------------ decoder-layer glue
+class FusedQuant:
+    """Arguments of a quantise fused into a glue call: codes q [rows, cols]
+    (uint8), the format and margin, an optional predicted bias, and one-element
+    int32 device tensors for the bias, amax bits and flags; ws is the op's
+    workspace (uint8 tensor)."""
+
+    def __init__(self, q, bias, ws, fmt=E4M3, margin=0, bias_pred=None, amax_bits=None, flags=None):
+        self.q, self.bias, self.ws = q, bias, ws
+        self.fmt, self.margin, self.bias_pred = fmt, margin, bias_pred
+        self.amax_bits, self.flags = amax_bits, flags
+
+    def args(self):
+        return (self.fmt, self.margin, _p(self.bias_pred), _p(self.bias), _p(self.amax_bits), _p(self.flags),
+                _p(self.q), _ld(self.q), _p(self.ws), self.ws.numel() * self.ws.element_size())
+
+
+_NO_QUANT = (E4M3, 0, None, None, None, None, None, 0, None, 0)
+
+
+def _bf16(t: torch.Tensor, name: str) -> None:
+    if t.dtype != torch.bfloat16:
+        raise TypeError(f"{name}: expected bfloat16, got {t.dtype}")
+
+
+def llama_rmsnorm_ws_bytes(rows: int) -> int:
+    return int(lib().llama_rmsnorm_ws_bytes(int(rows)))
+
+
+def llama_rmsnorm_quantise(x, g, eps=1e-5, res=None, h=None, y=None, fq: FusedQuant | None = None, stream=None):
+    """y = RMSNorm(x [+ res]) * g (and h = x + res), optionally with the fused
+    quantise of y.  Returns y."""
+    _bf16(x, "x")
+    rows, cols = x.shape
+    y = torch.empty((rows, cols), dtype=torch.bfloat16, device=x.device) if y is None else y
+    st = lib().llama_rmsnorm_quantise(_p(x), _ld(x), _p(res), _ld(res) if res is not None else 0, _p(g), rows,
+                                      cols, float(eps), _p(h), _ld(h) if h is not None else 0, _p(y), _ld(y),
+                                      *(fq.args() if fq else _NO_QUANT), _stream(stream))
+    _check("llama_rmsnorm_quantise", st)
+    return y
+
+
+def llama_rope_table(seq_len: int, d_head: int, theta: float = 10000.0, table=None, device=None, stream=None):
+    if table is None:
+        table = torch.empty(seq_len * d_head, dtype=torch.float32, device=device)
+    st = lib().llama_rope_table(int(seq_len), int(d_head), float(theta), _p(table), _stream(stream))
+    _check("llama_rope_table", st)
+    return table
+
+
+def llama_rope(x, n_heads: int, d_head: int, seq_len: int, table, stream=None):
+    """Rotary embedding in place on the first n_heads heads of x (a 2-D view
+    whose rows are contiguous, e.g. the Q and K columns of the QKV output)."""
+    _bf16(x, "x")
+    rows = x.shape[0]
+    ld = x.stride(0)
+    st = lib().llama_rope(_p(x), rows, ld, int(n_heads), int(d_head), int(seq_len), _p(table), _stream(stream))
+    _check("llama_rope", st)
+    return x
+
+
+def llama_attention_ws_bytes(rows: int, seq_len: int, n_heads: int) -> int:
+    return int(lib().llama_attention_ws_bytes(int(rows), int(seq_len), int(n_heads)))
+
+
+def llama_attention(qkv, seq_len: int, n_heads: int, n_kv_heads: int, d_head: int = 128, o=None,
+                    fq: FusedQuant | None = None, stream=None):
+    """Causal grouped-query attention over the QKV output; returns o."""
+    _bf16(qkv, "qkv")
+    rows = qkv.shape[0]
+    o = torch.empty((rows, n_heads * d_head), dtype=torch.bfloat16, device=qkv.device) if o is None else o
+    st = lib().llama_attention(_p(qkv), rows, _ld(qkv), int(seq_len), int(n_heads), int(n_kv_heads), int(d_head),
+                               _p(o), _ld(o), *(fq.args() if fq else _NO_QUANT), _stream(stream))
+    _check("llama_attention", st)
+    return o
+
+
+def llama_swiglu_ws_bytes() -> int:
+    return int(lib().llama_swiglu_ws_bytes())
+
+
+def llama_swiglu_quantise(gu, ffn: int, a=None, fq: FusedQuant | None = None, stream=None):
+    """a = silu(gate) * up over the fused gate+up output; returns a."""
+    _bf16(gu, "gu")
+    rows = gu.shape[0]
+    a = torch.empty((rows, ffn), dtype=torch.bfloat16, device=gu.device) if a is None else a
+    st = lib().llama_swiglu_quantise(_p(gu), _ld(gu), rows, int(ffn), _p(a), _ld(a),
+                                     *(fq.args() if fq else _NO_QUANT), _stream(stream))
+    _check("llama_swiglu_quantise", st)
+    return a
+
+
+def llama_residual_add(a, b, out=None, stream=None):
+    _bf16(a, "a")
+    out = torch.empty_like(a) if out is None else out
+    st = lib().llama_residual_add(_p(a), _p(b), _p(out), a.numel(), _stream(stream))
+    _check("llama_residual_add", st)
+    return out

@@ -30,7 +30,7 @@ class Tensor:
     name: str
     rows: int
     cols: int
-    kind: str            # "normal", "outlier_cols", "row_log2_uniform"
+    kind: str            # "normal", "outlier_cols", "row_log2_uniform", "gain"
     std: float = 1.0
     extra: tuple = ()
 
@@ -135,6 +135,70 @@ WORKLOADS = {
 }
 
 
+@dataclass(frozen=True)
+class LayerConfig:
+    """One Llama 2 decoder layer: the dimensions of Table 1, its four FP8
+    linears (App. E: QKV [d, (n_heads + 2 n_kv_heads) d_head], O
+    [n_heads d_head, d], gate+up [d, 2 ffn], down [ffn, d]) and a call of
+    `rows` tokens in sequences of `seq_len`."""
+    name: str
+    index: int           # seed base, after the linear workloads
+    description: str
+    d_model: int
+    n_heads: int
+    n_kv_heads: int
+    d_head: int
+    ffn: int
+    rows: int
+    seq_len: int
+    w_std: float = 0.01
+
+    def tensors(self) -> tuple:
+        d, q = self.d_model, self.n_heads * self.d_head
+        return (Tensor("H", self.rows, d, "normal", 1.0),
+                Tensor("g_attn", 1, d, "gain", 0.1), Tensor("g_mlp", 1, d, "gain", 0.1),
+                _w("Wqkv", d, (self.n_heads + 2 * self.n_kv_heads) * self.d_head, self.w_std),
+                _w("Wo", q, d, self.w_std), _w("Wgu", d, 2 * self.ffn, self.w_std),
+                _w("Wd", self.ffn, d, self.w_std))
+
+    def linears(self) -> tuple:
+        """(name, K, N) of the four linears, in call order."""
+        d = self.d_model
+        return (("qkv", d, (self.n_heads + 2 * self.n_kv_heads) * self.d_head),
+                ("o", self.n_heads * self.d_head, d), ("gate_up", d, 2 * self.ffn), ("down", self.ffn, d))
+
+
+LAYERS = {
+    # Llama 2 70B decoder layer (d 8192, 64 query / 8 key-value heads of 128,
+    # ffn 28672), post-training-quantised weights, prefill of one 2048-token
+    # sequence: input hidden state N(0,1), RMSNorm gains 1 + N(0, 0.1).
+    "llama2-70b-layer": LayerConfig(
+        "llama2-70b-layer", 5,
+        "Llama-2-70B decoder layer, PTQ inference, prefill 2048 tokens: H 2048x8192 N(0,1), "
+        "W QKV 8192x10240, O 8192x8192, gate+up 8192x57344, down 28672x8192 N(0,0.01), "
+        "RMSNorm gains 1+N(0,0.1); GQA 64/8 heads of 128, causal",
+        8192, 64, 8, 128, 28672, 2048, 2048),
+    # Llama 2 7B decoder layer (32 heads, no grouping), two 2048-token sequences.
+    "llama2-7b-layer": LayerConfig(
+        "llama2-7b-layer", 6,
+        "Llama-2-7B decoder layer, PTQ inference, prefill 2x2048 tokens: H 4096x4096 N(0,1), "
+        "W QKV 4096x12288, O 4096x4096, gate+up 4096x22016, down 11008x4096 N(0,0.02); 32 heads of 128",
+        4096, 32, 32, 128, 11008, 4096, 2048, 0.02),
+    # Small layer for parity against the oracle: grouped heads (8 / 2), two
+    # sequences of 150 tokens (ragged query and key blocks).
+    "tiny-layer": LayerConfig(
+        "tiny-layer", 7, "small decoder layer for parity: d 512, 8/2 heads of 128, ffn 1408, 2x150 tokens",
+        512, 8, 2, 128, 1408, 300, 150, 0.05),
+}
+
+
+def make_layer_tensor(cfg: LayerConfig, name: str) -> torch.Tensor:
+    ts = cfg.tensors()
+    idx = [t.name for t in ts].index(name)
+    t = ts[idx]
+    return draw(t.rows, t.cols, t.kind, t.std, t.extra, 1000 * cfg.index + idx)
+
+
 def base_seed(w: Workload) -> int:
     return 1000 * w.index
 
@@ -162,6 +226,8 @@ def draw(rows: int, cols: int, kind: str = "normal", std: float = 1.0, extra: tu
         lo, hi = extra
         u = torch.rand((rows, 1), generator=g, dtype=torch.float64) * (hi - lo) + lo
         x.mul_(torch.exp2(u).to(torch.float32))
+    elif kind == "gain":            # RMSNorm gain: 1 + N(0, std)
+        x.add_(1.0)
     elif kind != "normal":
         raise ValueError(kind)
     return x.to(torch.bfloat16)

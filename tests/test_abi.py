@@ -177,3 +177,57 @@ def test_segments_mode_rows_reject(L):
     assert h(FAKE, 4, FAKE, 3, NULL, NULL) == F.EINVAL     # count
     assert h(NULL, 4, FAKE, 3, FAKE, NULL) == F.EINVAL     # biases
     assert h(NULL, 0, FAKE, 3, FAKE, NULL) == F.OK         # nothing to count
+
+
+def test_decoder_glue_workspace_sizes(L):
+    assert L.llama_rmsnorm_ws_bytes(0) == 0
+    assert L.llama_rmsnorm_ws_bytes(2048) == 4 * (1 + 2048)
+    assert L.llama_swiglu_ws_bytes() == 4 * (1 + 2048)
+    # one maximum per (query head, sequence, block of 128 queries)
+    assert L.llama_attention_ws_bytes(2048, 2048, 64) == 4 * (1 + 64 * 16)
+    assert L.llama_attention_ws_bytes(300, 150, 8) == 4 * (1 + 8 * 2 * 2)
+    assert L.llama_attention_ws_bytes(0, 16, 8) == 0
+
+
+def test_decoder_glue_rejects(L):
+    A = ctypes.c_void_p(0x100000)
+    ws = 4 * 4097
+    # llama_rmsnorm_quantise(x, ldx, res, ldr, g, rows, cols, eps, h, ldh, y, ldy, fmt, margin, pred, bias,
+    #                        amax, flags, q, ldq, ws, ws_bytes, stream)
+    ok = [A, 64, NULL, 0, A, 4, 64, 1e-5, NULL, 0, A, 64, 0, 0, NULL, A, NULL, NULL, A, 64, A, ws, NULL]
+    for i, bad in ((0, NULL), (0, ctypes.c_void_p(0x100008)), (1, 60), (1, 68), (4, NULL), (6, 12), (7, -1.0),
+                   (7, float("nan")), (10, NULL), (11, 32), (12, 9), (15, NULL), (18, ODD), (19, 60),
+                   (20, NULL), (21, 8), (5, -1)):
+        args = list(ok)
+        args[i] = bad
+        assert L.llama_rmsnorm_quantise(*args) == F.EINVAL, (i, bad)
+    # llama_attention(qkv, rows, ld, seq_len, nh, nkv, dh, o, ldo, fmt, margin, pred, bias, amax, flags, q, ldq,
+    #                 ws, ws_bytes, stream)
+    ok = [A, 256, 12 * 128, 256, 8, 2, 128, A, 8 * 128, 0, 0, NULL, A, NULL, NULL, NULL, 0, NULL, 0, NULL]
+    for i, bad, st in ((6, 64, F.ENOTSUP), (5, 3, F.EINVAL), (4, 0, F.EINVAL), (3, 0, F.EINVAL),
+                       (2, 11 * 128, F.EINVAL), (8, 7 * 128, F.EINVAL), (0, NULL, F.EINVAL), (7, ODD, F.EINVAL)):
+        args = list(ok)
+        args[i] = bad
+        assert L.llama_attention(*args) == st, (i, bad)
+    # with codes requested, the quantise arguments are checked too
+    args = list(ok)
+    args[15], args[16], args[17], args[18] = A, 8 * 128, A, 8   # workspace too small
+    assert L.llama_attention(*args) == F.EINVAL
+    # llama_swiglu_quantise(gu, ldgu, rows, ffn, a, lda, fmt, margin, pred, bias, amax, flags, q, ldq, ws, ws_bytes, s)
+    ok = [A, 2816, 16, 1408, A, 1408, 0, 0, NULL, NULL, NULL, NULL, NULL, 0, NULL, 0, NULL]
+    for i, bad in ((3, 1404), (1, 2808), (5, 1400), (0, NULL), (4, ODD)):
+        args = list(ok)
+        args[i] = bad
+        assert L.llama_swiglu_quantise(*args) == F.EINVAL, (i, bad)
+    # llama_rope(x, rows, ld, n_heads, d_head, seq_len, table, stream); llama_rope_table(seq, dh, theta, table, s)
+    assert L.llama_rope(A, 4, 1024, 8, 120, 4, A, NULL) == F.EINVAL     # d_head not a multiple of 16
+    assert L.llama_rope(A, 4, 1000, 8, 128, 4, A, NULL) == F.EINVAL     # row stride
+    assert L.llama_rope(A, 4, 1024, 8, 128, 0, A, NULL) == F.EINVAL     # seq_len
+    assert L.llama_rope(A, 4, 1024, 8, 128, 4, NULL, NULL) == F.EINVAL  # table
+    assert L.llama_rope(NULL, 0, 1024, 8, 128, 4, NULL, NULL) == F.OK   # nothing to rotate
+    assert L.llama_rope_table(16, 128, -1.0, A, NULL) == F.EINVAL
+    assert L.llama_rope_table(0, 128, 1e4, A, NULL) == F.EINVAL
+    # llama_residual_add(a, b, out, n, stream)
+    assert L.llama_residual_add(A, A, A, 12, NULL) == F.EINVAL
+    assert L.llama_residual_add(A, ODD, A, 16, NULL) == F.EINVAL
+    assert L.llama_residual_add(NULL, NULL, NULL, 0, NULL) == F.OK
