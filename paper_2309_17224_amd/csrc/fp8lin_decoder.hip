@@ -296,49 +296,51 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
     const int t = bid / p.nh;
     const int qb = p.nqb - 1 - t / p.nseq;
     const int64_t s0 = (int64_t)(t % p.nseq) * p.seq_len;
-    const int64_t s_end = s0 + p.seq_len < p.rows ? s0 + p.seq_len : p.rows;
-    const int64_t q0 = s0 + (int64_t)qb * kBq;
+    // Positions within the sequence (32-bit): queries q0 .., keys 0 .. kend-1.
+    const int slen = (int)(s0 + p.seq_len < p.rows ? p.seq_len : p.rows - s0);
+    const int q0 = qb * kBq;
 
     const bool cast = QUANT && p.pred;
     const int bq = QUANT ? fused_bias(p.pred, p.used) : 0;
-    if (q0 >= s_end) {  // a block past the end of a short last sequence
+    if (q0 >= slen) {  // a block past the end of a short last sequence
         if (QUANT && tid == 0) p.parts[bid] = 0u;
         return;
     }
     const int hk = h / (p.nh / p.nkv);
-    const uint16_t* Qg = p.qkv + (int64_t)h * kHd;
-    const uint16_t* Kg = p.qkv + (int64_t)(p.nh + hk) * kHd;
-    const uint16_t* Vg = p.qkv + (int64_t)(p.nh + p.nkv + hk) * kHd;
-    const int64_t kend = q0 + kBq < s_end ? q0 + kBq : s_end;  // keys s0 .. kend - 1
-    const int nkb = (int)((kend - s0 + kBk - 1) / kBk);
-    const int64_t wq0 = q0 + 32 * w;
+    const uint16_t* Qg = p.qkv + s0 * p.ld + (int64_t)h * kHd;
+    const uint16_t* Kg = p.qkv + s0 * p.ld + (int64_t)(p.nh + hk) * kHd;
+    const uint16_t* Vg = p.qkv + s0 * p.ld + (int64_t)(p.nh + p.nkv + hk) * kHd;
+    const int kend = q0 + kBq < slen ? q0 + kBq : slen;
+    const int nkb = (kend + kBk - 1) / kBk;
+    const int wq0 = q0 + 32 * w;
 
-    // Query fragments (B operand of S^T = K . Q^T): Q[q][32 ds + 8 g .. + 7].
+    // Query fragments (B operand of S^T = K . Q^T): Q[q][32 ds + 8 g .. + 7];
+    // rows past the end read the last row (their outputs are not stored).
     u32x4 qf[2][4];
 #pragma unroll
     for (int qt = 0; qt < 2; ++qt) {
-        const int64_t row = wq0 + 16 * qt + l16;
+        const int row = min(wq0 + 16 * qt + l16, slen - 1);
 #pragma unroll
-        for (int ds = 0; ds < 4; ++ds)
-            qf[qt][ds] = row < s_end ? ldg16(Qg + row * p.ld + 32 * ds + 8 * g) : u32x4{0u, 0u, 0u, 0u};
+        for (int ds = 0; ds < 4; ++ds) qf[qt][ds] = ldg16(Qg + (int64_t)row * p.ld + 32 * ds + 8 * g);
     }
 
     // Staging roles: K as four 16-byte chunks per lane (key idx/16, chunk
     // idx%16); V as keys 4u .. 4u+3 x columns 8v .. 8v+7 (u = tid/16, v = tid%16).
+    // Rows past kend read row kend-1 (a finite copy; those keys are masked).
     const int vu = tid >> 4, vv = tid & 15;
     u32x4 kreg[4], vreg[4];
     auto load_block = [&](int kb) {
-        const int64_t kbase = s0 + (int64_t)kb * kBk;
+        const int kbase = kb * kBk;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int idx = tid + kThreads * j;
-            const int64_t row = kbase + (idx >> 4);
-            kreg[j] = row < kend ? ldg16(Kg + row * p.ld + (idx & 15) * 8) : u32x4{0u, 0u, 0u, 0u};
+            const int row = min(kbase + (idx >> 4), kend - 1);
+            kreg[j] = ldg16(Kg + (int64_t)row * p.ld + (idx & 15) * 8);
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int64_t row = kbase + 4 * vu + j;
-            vreg[j] = row < kend ? ldg16(Vg + row * p.ld + 8 * vv) : u32x4{0u, 0u, 0u, 0u};
+            const int row = min(kbase + 4 * vu + j, kend - 1);
+            vreg[j] = ldg16(Vg + (int64_t)row * p.ld + 8 * vv);
         }
     };
     // K: rows of 256 bytes, 16-byte chunk c of key k at chunk c ^ (k mod 16).
@@ -371,15 +373,24 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt)
         for (int qt = 0; qt < 2; ++qt) o[dt][qt] = f4_t{0.f, 0.f, 0.f, 0.f};
+    // Running maximum of the raw scores and per-lane partial row sums.
     float mrun[2] = {-INFINITY, -INFINITY}, lsum[2] = {0.f, 0.f};
+    const float c2 = p.scale_log2;
 
     load_block(0);
     store_block(0);
+    // Every load of the prologue (the query fragments included) has landed:
+    // the loop's waits then only cover the loads issued inside the loop.
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     for (int kb = 0; kb < nkb; ++kb) {
         const int buf = kb & 1;
-        if (kb + 1 < nkb) load_block(kb + 1);
-        const int64_t kbase = s0 + (int64_t)kb * kBk;
+        // The next block's loads, unconditionally (the last iteration reloads
+        // its own block into the other buffer, which nothing reads): a load
+        // that could reach the back-edge unconsumed would make the compiler
+        // wait for these loads in the middle of the matrix work.
+        load_block(kb + 1 < nkb ? kb + 1 : kb);
+        const int kbase = kb * kBk;
         if (kbase <= wq0 + 31) {  // some key of the block is visible to some query of this wave
             const uint8_t* Kl = lds + buf * 2 * kKvBytes;
             const uint8_t* Vl = Kl + kKvBytes;
@@ -396,38 +407,48 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
                     s[kt][0] = mfma_bf16(kf, qf[0][ds], s[kt][0]);
                     s[kt][1] = mfma_bf16(kf, qf[1][ds], s[kt][1]);
                 }
-            const bool mask = (kbase + kBk - 1 > wq0) || (kbase + kBk > kend);
+            // keys above a query's position, or past the end: -inf (wave-uniform test)
+            if (kbase + kBk - 1 > wq0 || kbase + kBk > kend) {
+#pragma unroll
+                for (int qt = 0; qt < 2; ++qt) {
+                    const int q = wq0 + 16 * qt + l16;
+#pragma unroll
+                    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const int key = kbase + kt * 16 + 4 * g + i;
+                            s[kt][qt][i] = (key > q || key >= kend) ? -INFINITY : s[kt][qt][i];
+                        }
+                }
+            }
             u32x4 pf[2][2];
 #pragma unroll
             for (int qt = 0; qt < 2; ++qt) {
-                const int64_t qrow = wq0 + 16 * qt + l16;
                 float mx = -INFINITY;
 #pragma unroll
                 for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        float v = s[kt][qt][i] * p.scale_log2;
-                        if (mask) {
-                            const int64_t key = kbase + kt * 16 + 4 * g + i;
-                            if (key > qrow || key >= kend) v = -INFINITY;
-                        }
-                        s[kt][qt][i] = v;
-                        mx = fmaxf(mx, v);
-                    }
+                    for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[kt][qt][i]);
                 mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
                 mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
                 const float mnew = fmaxf(mrun[qt], mx);
-                const float alpha = exp2f(mrun[qt] - mnew);
+                // alpha = 1 exactly when the maximum did not grow; then the
+                // rescale is skipped (multiplying by 1 changes nothing)
+                const float alpha = __builtin_amdgcn_exp2f((mrun[qt] - mnew) * c2);
                 mrun[qt] = mnew;
-                float ls = lsum[qt] * alpha;
+                if (__any(alpha != 1.0f)) {
+                    lsum[qt] *= alpha;
 #pragma unroll
-                for (int dt = 0; dt < 8; ++dt) o[dt][qt] *= alpha;
+                    for (int dt = 0; dt < 8; ++dt) o[dt][qt] *= alpha;
+                }
+                const float moff = -mnew * c2;
                 float pr[4][4];
+                float ls = lsum[qt];
 #pragma unroll
                 for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        pr[kt][i] = exp2f(s[kt][qt][i] - mnew);
+                        pr[kt][i] = __builtin_amdgcn_exp2f(fmaf(s[kt][qt][i], c2, moff));
                         ls += pr[kt][i];
                     }
                 lsum[qt] = ls;
@@ -448,7 +469,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
                 }
             }
         }
-        if (kb + 1 < nkb) store_block(buf ^ 1);
+        store_block(buf ^ 1);
         __syncthreads();
     }
 
@@ -472,17 +493,19 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
     }
     __syncthreads();
     uint32_t mag = 0;
+    uint16_t* Og = p.o + s0 * p.ldo + (int64_t)h * kHd;
+    uint8_t* Q8 = QUANT ? p.q8 + s0 * p.ldq + (int64_t)h * kHd : nullptr;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         const int idx = tid + kThreads * j;
         const int r = idx >> 4, c = idx & 15;
-        const int64_t qrow = q0 + r;
-        if (qrow >= s_end) continue;
+        const int q = q0 + r;
+        if (q >= slen) continue;
         const uint4 v = *(const uint4*)(lds + r * 256 + ((c ^ (r & 15)) << 4));
-        st16(p.o + qrow * p.ldo + (int64_t)h * kHd + 8 * c, v);
+        st16(Og + (int64_t)q * p.ldo + 8 * c, v);
         if (QUANT) {
             mag = max(mag, mag8(v));
-            if (cast) *(uint2*)(p.q8 + qrow * p.ldq + (int64_t)h * kHd + 8 * c) = codes8<FMT>(v, bq);
+            if (cast) *(uint2*)(Q8 + (int64_t)q * p.ldq + 8 * c) = codes8<FMT>(v, bq);
         }
     }
     if (QUANT) {
