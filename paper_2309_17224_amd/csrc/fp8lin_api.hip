@@ -397,6 +397,7 @@ int32_t llama_attention(const void* qkv, int64_t rows, int64_t ld, int64_t seq_l
     if (!rows_ok(ld, (int64_t)(n_heads + 2 * n_kv_heads) * d_head) || !rows_ok(ldo, cols)) return FP8_EINVAL;
     if (glue_parts_attention(rows, seq_len, n_heads) > INT32_MAX) return FP8_ENOTSUP;
     if ((seq_len < rows ? seq_len : rows) > ((int64_t)1 << 30)) return FP8_ENOTSUP;  // positions are 32-bit
+    if (ld > ((int64_t)1 << 24)) return FP8_ENOTSUP;  // 32-bit offsets within a block of 64 rows
     const int32_t st = glue_quant(fmt, margin, bias_pred, bias, amax_bits, flags, q, ldq, cols, ws, ws_bytes,
                                   1 + glue_parts_attention(rows, seq_len, n_heads), &fq);
     if (st != FP8_OK) return st;

@@ -253,9 +253,12 @@ __global__ __launch_bounds__(kThreads) void swiglu_kernel(
 //                  (keys 4g..4g+3 and 16+4g..16+4g+3 of a 32-key slice for
 //                  lane group g), A = V^T read from an LDS copy of V stored
 //                  transposed with the keys of each slice permuted to match.
-// Online softmax in fp32 with base-2 exponentials (scores pre-scaled by
-// log2(e) / sqrt(128)); P is rounded to bf16 for the second product; the row
-// sums are kept per lane and reduced once at the end.
+// Online softmax in fp32 with base-2 exponentials (the scale log2(e) /
+// sqrt(128) folded into the exponent's FMA); the exponent offset follows the
+// running maximum lazily (moved only when it is exceeded by 8 in log2 units,
+// so the probabilities stay below 256 and O is rarely rescaled); P is rounded
+// to bf16 for the second product; the row sums are kept per lane and reduced
+// once at the end.
 constexpr int kHd = 128, kBq = 128, kBk = 64;
 constexpr int kKvBytes = kBk * kHd * 2;  // one K or V block in LDS: 16 KiB
 
@@ -279,6 +282,10 @@ __device__ __forceinline__ f4_t mfma_bf16(u32x4 a, u32x4 b, f4_t c) {
 }
 
 __device__ __forceinline__ u32x4 ldg16(const uint16_t* p) { return *(const u32x4*)p; }
+
+// Placement of row d of the transposed V block (see the attention kernel).
+__device__ __forceinline__ int vt_row(int d) { return d ^ ((d >> 5) & 1); }
+__device__ __forceinline__ int vt_swz(int d) { return ((d >> 1) ^ (d >> 3)) & 7; }
 
 template <bool QUANT, int FMT>
 __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
@@ -327,26 +334,44 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
     // Staging roles: K as four 16-byte chunks per lane (key idx/16, chunk
     // idx%16); V as keys 4u .. 4u+3 x columns 8v .. 8v+7 (u = tid/16, v = tid%16).
     // Rows past kend read row kend-1 (a finite copy; those keys are masked).
-    const int vu = tid >> 4, vv = tid & 15;
+    // Full blocks: a wave-uniform block base plus per-lane 32-bit offsets
+    // (rows tid/16 + 16 j of K, 4 (tid/16) + j of V); the last, partial block
+    // clamps each row.
+    const int vu = w + 4 * ((tid >> 4) & 3), vv = tid & 15;
+    const int ld = (int)p.ld;
+    const int koff = (tid >> 4) * ld + (tid & 15) * 8, voff = 4 * vu * ld + 8 * vv;
     u32x4 kreg[4], vreg[4];
     auto load_block = [&](int kb) {
         const int kbase = kb * kBk;
+        const uint16_t* kp = Kg + (int64_t)kbase * p.ld;
+        const uint16_t* vp = Vg + (int64_t)kbase * p.ld;
+        if (kbase + kBk <= kend) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int idx = tid + kThreads * j;
-            const int row = min(kbase + (idx >> 4), kend - 1);
-            kreg[j] = ldg16(Kg + (int64_t)row * p.ld + (idx & 15) * 8);
-        }
+            for (int j = 0; j < 4; ++j) kreg[j] = ldg16(kp + koff + 16 * j * ld);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int row = min(kbase + 4 * vu + j, kend - 1);
-            vreg[j] = ldg16(Vg + (int64_t)row * p.ld + 8 * vv);
+            for (int j = 0; j < 4; ++j) vreg[j] = ldg16(vp + voff + j * ld);
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int idx = tid + kThreads * j;
+                const int row = min(kbase + (idx >> 4), kend - 1) - kbase;
+                kreg[j] = ldg16(kp + row * ld + (idx & 15) * 8);
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int row = min(kbase + 4 * vu + j, kend - 1) - kbase;
+                vreg[j] = ldg16(vp + row * ld + 8 * vv);
+            }
         }
     };
     // K: rows of 256 bytes, 16-byte chunk c of key k at chunk c ^ (k mod 16).
     // V^T: rows of 128 bytes (one per column d), 64 keys each in permuted
     // order: key 32 s + kk sits at 32 s + 8 ((kk mod 16) / 4) + 4 (kk / 16) +
-    // kk mod 4; 16-byte chunk c of row d at chunk c ^ ((d / 2) mod 8).
+    // kk mod 4; row d is stored at row vt_row(d), its 16-byte chunk c at chunk
+    // c ^ vt_swz(d).  With the lanes of a wave staging keys of both halves of
+    // a slice (vu = wave + 4 (lane / 16)), every 8-byte write instruction
+    // spreads evenly over the 64 banks and every fragment read is
+    // conflict-free (checked against the measured ds_read_b128 phases).
     auto store_block = [&](int buf) {
         uint8_t* Kl = lds + buf * 2 * kKvBytes;
         uint8_t* Vl = Kl + kKvBytes;
@@ -364,8 +389,8 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
             const int d0 = 8 * vv + 2 * m, d1 = d0 + 1;
             const uint2 e0 = make_uint2((r0 & 0xFFFFu) | (r1 << 16), (r2 & 0xFFFFu) | (r3 << 16));
             const uint2 e1 = make_uint2((r0 >> 16) | (r1 & 0xFFFF0000u), (r2 >> 16) | (r3 & 0xFFFF0000u));
-            *(uint2*)(Vl + d0 * 128 + ((cb ^ ((d0 >> 1) & 7)) << 4) + ob) = e0;
-            *(uint2*)(Vl + d1 * 128 + ((cb ^ ((d1 >> 1) & 7)) << 4) + ob) = e1;
+            *(uint2*)(Vl + vt_row(d0) * 128 + ((cb ^ vt_swz(d0)) << 4) + ob) = e0;
+            *(uint2*)(Vl + vt_row(d1) * 128 + ((cb ^ vt_swz(d1)) << 4) + ob) = e1;
         }
     };
 
@@ -376,6 +401,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
     // Running maximum of the raw scores and per-lane partial row sums.
     float mrun[2] = {-INFINITY, -INFINITY}, lsum[2] = {0.f, 0.f};
     const float c2 = p.scale_log2;
+    const float lazy = 8.0f / c2;  // 2^8 in probability, in units of raw scores
 
     load_block(0);
     store_block(0);
@@ -431,16 +457,20 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
                     for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[kt][qt][i]);
                 mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
                 mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-                const float mnew = fmaxf(mrun[qt], mx);
-                // alpha = 1 exactly when the maximum did not grow; then the
-                // rescale is skipped (multiplying by 1 changes nothing)
-                const float alpha = __builtin_amdgcn_exp2f((mrun[qt] - mnew) * c2);
-                mrun[qt] = mnew;
-                if (__any(alpha != 1.0f)) {
+                // The exponent offset moves only when a score exceeds it by
+                // more than 2^8 in probability (the first block always): the
+                // probabilities stay below 256, and the rescale of the sums
+                // and of O by alpha is rare.
+                const bool grow = mx > mrun[qt] + lazy;
+                if (__any(grow)) {
+                    const float mnew = grow ? mx : mrun[qt];
+                    const float alpha = __builtin_amdgcn_exp2f((mrun[qt] - mnew) * c2);
+                    mrun[qt] = mnew;
                     lsum[qt] *= alpha;
 #pragma unroll
                     for (int dt = 0; dt < 8; ++dt) o[dt][qt] *= alpha;
                 }
+                const float mnew = mrun[qt];
                 const float moff = -mnew * c2;
                 float pr[4][4];
                 float ls = lsum[qt];
@@ -463,7 +493,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
                 const int d = dt * 16 + l16;
 #pragma unroll
                 for (int ks = 0; ks < 2; ++ks) {
-                    const u32x4 vf = *(const u32x4*)(Vl + d * 128 + (((4 * ks + g) ^ ((d >> 1) & 7)) << 4));
+                    const u32x4 vf = *(const u32x4*)(Vl + vt_row(d) * 128 + (((4 * ks + g) ^ vt_swz(d)) << 4));
                     o[dt][0] = mfma_bf16(vf, pf[0][ks], o[dt][0]);
                     o[dt][1] = mfma_bf16(vf, pf[1][ks], o[dt][1]);
                 }
