@@ -258,7 +258,8 @@ __global__ __launch_bounds__(kThreads) void swiglu_kernel(
 // running maximum lazily (moved only when it is exceeded by 8 in log2 units,
 // so the probabilities stay below 256 and O is rarely rescaled); P is rounded
 // to bf16 for the second product; the row sums are kept per lane and reduced
-// once at the end.
+// once at the end.  A query row that sees no key of a block (above the
+// diagonal) gets maximum -inf there, no rescale and zero weights.
 constexpr int kHd = 128, kBq = 128, kBk = 64;
 constexpr int kKvBytes = kBk * kHd * 2;  // one K or V block in LDS: 16 KiB
 
@@ -282,6 +283,24 @@ __device__ __forceinline__ f4_t mfma_bf16(u32x4 a, u32x4 b, f4_t c) {
 }
 
 __device__ __forceinline__ u32x4 ldg16(const uint16_t* p) { return *(const u32x4*)p; }
+
+// Maximum / sum over lanes l, l ^ 16, l ^ 32, l ^ 48 (the four lanes that hold
+// one query's scores) with VALU lane swaps: swapping a value with itself
+// between rows 0-1 and 2-3 of 16 lanes (then between the two halves of the
+// wave) leaves each lane holding its own value and its partner's, in some
+// order, which a symmetric operation does not see.
+__device__ __forceinline__ float quad_max(float v) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float quad_sum(float v) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
 
 // Placement of row d of the transposed V block (see the attention kernel).
 __device__ __forceinline__ int vt_row(int d) { return d ^ ((d >> 5) & 1); }
@@ -417,7 +436,11 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
         // wait for these loads in the middle of the matrix work.
         load_block(kb + 1 < nkb ? kb + 1 : kb);
         const int kbase = kb * kBk;
-        if (kbase <= wq0 + 31) {  // some key of the block is visible to some query of this wave
+        // Every wave runs every block: one entirely above a wave's diagonal
+        // (at most 2 of 4 waves, in the last block) is masked to zero weight,
+        // which costs less than the accumulator copies a skip branch makes
+        // the compiler insert.
+        {
             const uint8_t* Kl = lds + buf * 2 * kKvBytes;
             const uint8_t* Vl = Kl + kKvBytes;
             f4_t s[4][2];
@@ -455,8 +478,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
                 for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
                     for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[kt][qt][i]);
-                mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-                mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+                mx = quad_max(mx);
                 // The exponent offset moves only when a score exceeds it by
                 // more than 2^8 in probability (the first block always): the
                 // probabilities stay below 256, and the rescale of the sums
@@ -488,11 +510,13 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
                                        pack_bf16x2(pr[2 * ks + 1][0], pr[2 * ks + 1][1]),
                                        pack_bf16x2(pr[2 * ks + 1][2], pr[2 * ks + 1][3])};
             }
+            // key slices outer: successive products into one accumulator are
+            // 16 instructions apart
 #pragma unroll
-            for (int dt = 0; dt < 8; ++dt) {
-                const int d = dt * 16 + l16;
+            for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
-                for (int ks = 0; ks < 2; ++ks) {
+                for (int dt = 0; dt < 8; ++dt) {
+                    const int d = dt * 16 + l16;
                     const u32x4 vf = *(const u32x4*)(Vl + vt_row(d) * 128 + (((4 * ks + g) ^ vt_swz(d)) << 4));
                     o[dt][0] = mfma_bf16(vf, pf[0][ks], o[dt][0]);
                     o[dt][1] = mfma_bf16(vf, pf[1][ks], o[dt][1]);
@@ -508,10 +532,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
     // 256-byte rows of this head, cast with the fused bias on the way.
 #pragma unroll
     for (int qt = 0; qt < 2; ++qt) {
-        float ls = lsum[qt];
-        ls += __shfl_xor(ls, 16, 64);
-        ls += __shfl_xor(ls, 32, 64);
-        const float inv = 1.0f / ls;
+        const float inv = 1.0f / quad_sum(lsum[qt]);
         const int r = 32 * w + 16 * qt + l16;
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt) {
