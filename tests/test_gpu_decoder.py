@@ -234,3 +234,59 @@ def test_glue_rejects_bad_arguments(gpu):
         F.llama_attention(qkv, 4, 3, 2, 128)                         # 2 does not divide 3
     with pytest.raises(F.Fp8Error):
         F.llama_swiglu_quantise(torch.zeros((2, 20), dtype=torch.bfloat16, device=gpu), 10)
+
+
+# ---------------------------------------------------------------- edge cases
+def test_glue_empty_outputs_give_zero_bias_and_flag(gpu):
+    # an empty output with the quantise asked for: amax 0, bias 0, FLAG_ZERO (as fp8_quantise)
+    for make in (
+        lambda fq: F.llama_rmsnorm_quantise(torch.zeros((0, 64), dtype=torch.bfloat16, device=gpu),
+                                            torch.ones(64, dtype=torch.bfloat16, device=gpu), fq=fq),
+        lambda fq: F.llama_swiglu_quantise(torch.zeros((0, 64), dtype=torch.bfloat16, device=gpu), 32, fq=fq),
+        lambda fq: F.llama_attention(torch.zeros((0, 3 * 128), dtype=torch.bfloat16, device=gpu), 16, 1, 1, 128,
+                                     fq=fq),
+    ):
+        fq, scal = quant_args(gpu, 64, 1, 64, pred=5)
+        scal.fill_(-7)
+        make(fq)
+        torch.cuda.synchronize()
+        assert scal.cpu().tolist() == [0, 0, F.FLAG_ZERO]
+
+
+def test_rmsnorm_zero_and_nonfinite_rows(gpu, orc):
+    rows, cols = 6, 256
+    x = rand_bits((rows, cols), 301)
+    x[1] = 0                      # all-zero row: y = 0 (the eps keeps the scale finite)
+    x[3, 17] = 0x7F80             # +inf: the mean square is inf, the row scales by 0, inf * 0 = NaN
+    x[4, 5] = 0x7FC1              # NaN propagates through the row's mean square
+    g = rand_bits((1, cols), 302)[0]
+    _, y_ref = D.rmsnorm(x, g)
+    fq, scal = quant_args(gpu, F.llama_rmsnorm_ws_bytes(rows), rows, cols, pred=2)
+    y = np_bits(F.llama_rmsnorm_quantise(bf16_dev(x, gpu), bf16_dev(g, gpu), 1e-5, fq=fq))
+    torch.cuda.synchronize()
+    nan_g, nan_r = (y & 0x7FFF) > 0x7F80, (y_ref & 0x7FFF) > 0x7F80
+    assert np.array_equal(nan_g, nan_r)
+    assert np.all(y[1] & 0x7FFF == 0)
+    ulp_check(np.where(nan_g, 0, y).astype(np.uint16), np.where(nan_r, 0, y_ref).astype(np.uint16))
+    # the tensor holds NaN: the Eq. 3 bias is 0 with FLAG_NONFINITE, NaN codes are 0x7F with the sign
+    assert (i32(scal[0]), u32(scal[2])) == (0, F.FLAG_NONFINITE)
+    codes = fq.q.cpu().numpy()
+    assert np.all(codes[nan_g] & 0x7F == 0x7F)
+    q2, _, _, _, _ = F.fp8_quantise(bf16_dev(y, gpu), F.E4M3, 0)
+    assert np.array_equal(codes, q2.cpu().numpy())
+
+
+def test_swiglu_nonfinite(gpu, orc):
+    rows, ffn = 4, 64
+    gu = rand_bits((rows, 2 * ffn), 303)
+    gu[0, 3] = 0x7F80             # gate +inf: inf * sigmoid(inf) * u = +-inf
+    gu[1, 4] = 0xFF80             # gate -inf: -inf / (1 + inf) = NaN
+    gu[2, ffn + 7] = 0x7FC0       # up NaN
+    ref = D.swiglu(gu, ffn)
+    fq, scal = quant_args(gpu, F.llama_swiglu_ws_bytes(), rows, ffn, pred=0)
+    a = np_bits(F.llama_swiglu_quantise(bf16_dev(gu, gpu), ffn, fq=fq))
+    torch.cuda.synchronize()
+    nan_g, nan_r = (a & 0x7FFF) > 0x7F80, (ref & 0x7FFF) > 0x7F80
+    assert np.array_equal(nan_g, nan_r)
+    assert np.array_equal(a[~nan_g] & 0x7FFF == 0x7F80, ref[~nan_r] & 0x7FFF == 0x7F80)   # same infinities
+    assert (i32(scal[0]), u32(scal[2])) == (0, F.FLAG_NONFINITE)
