@@ -63,6 +63,10 @@ def parse():
     p.add_argument("--launch", choices=("graph", "eager"), default="graph",
                    help="timed steps: replays of one HIP graph holding the whole step, or "
                         "one host call per library call")
+    p.add_argument("--bias-per", choices=("tensor", "sequence"), default="tensor",
+                   help="decoder-layer workloads: one activation bias per tensor and call (quantise fused "
+                        "into the producing kernels), or one per sequence (segmented quantise, per-row-bias "
+                        "matmuls)")
     p.add_argument("--copy-mb", type=int, default=0,
                    help="only run a plain device-to-device copy of this many MB, --steps times "
                         "(reference kernel for scaling hardware traffic counters), then exit")
@@ -296,7 +300,7 @@ def bench_layer(args, cfg):
     cpu = {t.name: wl.make_layer_tensor(cfg, t.name) for t in cfg.tensors()}
     log(f"[bench] generated {len(cpu)} tensors in {time.time() - t0:.1f}s")
     W = {k: v.to(dev) for k, v in cpu.items() if k != "H"}
-    layer = DL.DecoderLayer(cfg, W, dev)
+    layer = DL.DecoderLayer(cfg, W, dev, bias_per=args.bias_per)
     layer.H.copy_(cpu["H"].to(dev))
     del W
     torch.cuda.synchronize()
@@ -326,7 +330,7 @@ def bench_layer(args, cfg):
                    "linears": [dict(name=n, M=cfg.rows, K=K, N=N) for n, K, N in cfg.linears()],
                    "mode": "PTQ inference, one decoder layer fwd (four FP8 linears; RMSNorm, RoPE, "
                            "attention, SwiGLU in bf16 with fused FP8-AMAX quantise)",
-                   "accumulate": "fp32", "outputs": "bf16",
+                   "accumulate": "fp32", "outputs": "bf16", "activation_bias": f"per {args.bias_per}",
                    "launch": ("one HIP graph replay per layer call" if args.launch == "graph"
                               else "one host call per library call")},
         "frac_of_fp8_peak": round(value / FP8_PEAK_TFLOPS, 4),

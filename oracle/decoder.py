@@ -159,30 +159,69 @@ def quantise(x: np.ndarray):
     return cast(np.ascontiguousarray(x), E4M3, b), b
 
 
+def quantise_per_sequence(x: np.ndarray, seq_len: int):
+    """FP8-AMAX of each sequence of seq_len consecutive rows as a tensor of its
+    own (the per-data-sample activation biases of App. D): returns (codes,
+    list of biases, bias of every row)."""
+    rows = x.shape[0]
+    q = np.empty(x.shape, dtype=np.uint8)
+    row_bias = np.empty(rows, dtype=np.int64)
+    biases = []
+    for s0 in range(0, rows, seq_len):
+        q[s0:s0 + seq_len], b = quantise(x[s0:s0 + seq_len])
+        row_bias[s0:s0 + seq_len] = b
+        biases.append(b)
+    return q, biases, row_bias
+
+
+def gemm_e4_rows(a8: np.ndarray, row_bias: np.ndarray, b8t: np.ndarray, bb: int) -> np.ndarray:
+    """gemm_e4 with one bias per row of a8: row m unscaled by 2^-(row_bias[m] + bb)."""
+    out = np.empty((a8.shape[0], b8t.shape[0]), dtype=np.uint16)
+    for v in np.unique(row_bias):
+        rows = np.nonzero(row_bias == v)[0]
+        out[rows] = gemm_e4(a8[rows], int(v), b8t, bb)
+    return out
+
+
 def layer_forward(H: np.ndarray, p: dict, seq_len: int, n_heads: int, n_kv_heads: int,
-                  d_head: int, ffn: int, eps: float = LLAMA_EPS) -> dict:
+                  d_head: int, ffn: int, eps: float = LLAMA_EPS, per_sequence: bool = False) -> dict:
     """One Llama 2 decoder layer, forward, with the four linears in FP8
     (App. E) and weights quantised beforehand (Sec. 3.1).  H is [rows, d]
     bf16 bits; p holds the RMSNorm gains g_attn, g_mlp (bf16 bits) and for
     each linear ("qkv", "o", "gate_up", "down") its transposed E4M3 codes
-    p[name + "_w8t"] ([N, K]) and bias p[name + "_bw"].  Returns every
-    intermediate tensor and activation bias, ending with "out"."""
+    p[name + "_w8t"] ([N, K]) and bias p[name + "_bw"].  Each activation that
+    enters a linear gets one bias for the whole call, or with per_sequence one
+    per sequence (then "b_*" are lists).  Returns every intermediate tensor and
+    activation bias, ending with "out"."""
     r = {}
     dq, dkv = n_heads * d_head, n_kv_heads * d_head
+
+    def quant(x):
+        if per_sequence:
+            q, biases, rb = quantise_per_sequence(x, seq_len)
+            return q, biases, rb
+        q, b = quantise(x)
+        return q, b, None
+
+    def lin(x8, b, rb, name):
+        if per_sequence:
+            return gemm_e4_rows(x8, rb, p[name + "_w8t"], p[name + "_bw"])
+        return gemm_e4(x8, b, p[name + "_w8t"], p[name + "_bw"])
+
     _, r["xn"] = rmsnorm(H, p["g_attn"], eps)
-    r["xn8"], r["b_xn"] = quantise(r["xn"])
-    r["qkv"] = gemm_e4(r["xn8"], r["b_xn"], p["qkv_w8t"], p["qkv_bw"])
+    r["xn8"], r["b_xn"], rb = quant(r["xn"])
+    r["qkv"] = lin(r["xn8"], r["b_xn"], rb, "qkv")
     r["q"] = rope(r["qkv"][:, :dq], seq_len, d_head)
     r["k"] = rope(r["qkv"][:, dq:dq + dkv], seq_len, d_head)
     r["v"] = r["qkv"][:, dq + dkv:dq + 2 * dkv]
     r["attn"] = attention(r["q"], r["k"], r["v"], seq_len, n_heads, n_kv_heads, d_head)
-    r["attn8"], r["b_attn"] = quantise(r["attn"])
-    r["o"] = gemm_e4(r["attn8"], r["b_attn"], p["o_w8t"], p["o_bw"])
+    r["attn8"], r["b_attn"], rb = quant(r["attn"])
+    r["o"] = lin(r["attn8"], r["b_attn"], rb, "o")
     r["h1"], r["hn"] = rmsnorm(r["o"], p["g_mlp"], eps, res=H)
-    r["hn8"], r["b_hn"] = quantise(r["hn"])
-    r["gu"] = gemm_e4(r["hn8"], r["b_hn"], p["gate_up_w8t"], p["gate_up_bw"])
+    r["hn8"], r["b_hn"], rb = quant(r["hn"])
+    r["gu"] = lin(r["hn8"], r["b_hn"], rb, "gate_up")
     r["act"] = swiglu(r["gu"], ffn)
-    r["act8"], r["b_act"] = quantise(r["act"])
-    r["down"] = gemm_e4(r["act8"], r["b_act"], p["down_w8t"], p["down_bw"])
+    r["act8"], r["b_act"], rb = quant(r["act"])
+    r["down"] = lin(r["act8"], r["b_act"], rb, "down")
     r["out"] = add(r["h1"], r["down"])
     return r

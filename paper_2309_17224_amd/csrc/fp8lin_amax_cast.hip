@@ -421,7 +421,7 @@ __global__ void fill_words_kernel(uint32_t* __restrict__ p, int64_t n, uint32_t 
 // kSegRows consecutive rows, a wave one row at a time (16-byte loads across
 // the row); the row maxima are folded by runs of rows of one segment, one
 // atomic max per run.
-constexpr int kSegRows = 32, kSegThreads = 256;
+constexpr int kSegRows = 4, kSegThreads = 256;  // one row per wave: a few thousand rows fill the chip
 
 template <int DT>
 __global__ __launch_bounds__(kSegThreads) void seg_amax_kernel(const void* __restrict__ x, int64_t rows,

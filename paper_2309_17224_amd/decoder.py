@@ -20,6 +20,12 @@ Each fused quantise casts with the previous call's bias as a prediction and
 re-casts only if the exact bias differs, so the codes are always those of the
 exact FP8-AMAX bias.  Buffers are allocated once; a call launches kernels only
 and can be captured in a HIP graph.
+
+Bias granularity: one bias per activation tensor and call ("tensor"), or one
+per sequence of the call ("sequence": the per-data-sample activation biases of
+the paper's inference, App. D): then each glue kernel writes its bf16 output
+only, fp8_quantise_segments gives every sequence its own Eq. 3 bias and codes,
+and fp8_linear_fwd_rows unscales each output row by its sequence's bias.
 """
 from __future__ import annotations
 
@@ -51,6 +57,19 @@ class _Act:
         return F.FusedQuant(self.q, self.bias, self.ws, F.E4M3, 0, bias_pred=self.bias,
                             amax_bits=self.scal[1:2], flags=self.scal[2:3])
 
+    def segments(self, nseg, device):
+        """Per-sequence bias buffers: [nseg] biases, amax bits and flags, and
+        the bias of every row."""
+        i32 = dict(dtype=torch.int32, device=device)
+        self.seg_bias = torch.zeros(nseg, **i32)
+        self.seg_amax = torch.zeros(nseg, **i32)
+        self.seg_flags = torch.zeros(nseg, **i32)
+        self.row_bias = torch.zeros(self.x.shape[0], **i32)
+
+    def quantise_segments(self, offsets):
+        F.fp8_quantise_segments(self.x, offsets, F.E4M3, 0, bias=self.seg_bias, amax_bits=self.seg_amax,
+                                flags=self.seg_flags, row_bias=self.row_bias, q=self.q)
+
 
 class DecoderLayer:
     """Buffers and calls of one decoder layer for a fixed number of tokens.
@@ -61,7 +80,12 @@ class DecoderLayer:
     ``calls`` lists (label, kind, work, fn) in issue order; running them is
     one forward call of the layer on ``self.H``."""
 
-    def __init__(self, cfg: LayerConfig, weights: dict, device):
+    BIAS_PER = ("tensor", "sequence")
+
+    def __init__(self, cfg: LayerConfig, weights: dict, device, bias_per: str = "tensor"):
+        if bias_per not in self.BIAS_PER:
+            raise ValueError(f"bias_per must be one of {self.BIAS_PER}")
+        self.bias_per = bias_per
         self.cfg = c = cfg
         dev = self.dev = torch.device(device)
         R, d, nh, nkv, dh, ffn = c.rows, c.d_model, c.n_heads, c.n_kv_heads, c.d_head, c.ffn
@@ -92,8 +116,14 @@ class DecoderLayer:
         self.act = _Act(R, ffn, F.llama_swiglu_ws_bytes(), dev)
         self.down = torch.empty((R, d), **bf)
         self.out = torch.empty((R, d), **bf)
+        self.nseg = (R + c.seq_len - 1) // c.seq_len
+        self.offsets = torch.tensor([min(s * c.seq_len, R) for s in range(self.nseg + 1)], dtype=torch.int32,
+                                    device=dev)
+        if bias_per == "sequence":
+            for a in (self.xn, self.att, self.hn, self.act):
+                a.segments(self.nseg, dev)
         self.graph = None
-        self.calls = self._build()
+        self.calls = self._build_sequence() if bias_per == "sequence" else self._build()
 
     def bw(self, name):
         return self.wscal[name][0:1]
@@ -130,6 +160,47 @@ class DecoderLayer:
             ("residual", "glue", 6 * R * d, lambda: F.llama_residual_add(self.h1, self.down, out=self.out)),
         ]
 
+    def _build_sequence(self):
+        """The layer with one activation bias per sequence: glue kernels
+        without the fused quantise, then a segmented quantise and the matmul
+        with per-row biases."""
+        c = self.cfg
+        R, d, ffn = c.rows, c.d_model, c.ffn
+        att_flop = 4 * c.n_heads * c.d_head * sum(
+            (min(c.seq_len, R - s) * (min(c.seq_len, R - s) + 1)) // 2 for s in range(0, R, c.seq_len))
+
+        def quant(a: _Act, label):
+            n = a.x.numel()
+            return (f"quantise/seq {label}", "quantise", 2 * 2 * n + n, lambda: a.quantise_segments(self.offsets))
+
+        def lin(name, a: _Act, y):
+            K, N = a.x.shape[1], y.shape[1]
+            return (f"{name}", "gemm_fwd", 2 * R * N * K,
+                    lambda: F.fp8_linear_fwd_rows(a.q, a.row_bias, self.w8t[name], self.bw(name), y=y))
+
+        return [
+            ("rmsnorm attn", "glue", 2 * R * d + 2 * R * d,
+             lambda: F.llama_rmsnorm_quantise(self.H, self.g_attn, LLAMA_EPS, y=self.xn.x)),
+            quant(self.xn, "attn input"),
+            lin("qkv", self.xn, self.qkv),
+            ("rope", "glue", 4 * R * (self.dq + self.dkv),
+             lambda: F.llama_rope(self.qkv[:, :self.dq + self.dkv], c.n_heads + c.n_kv_heads, c.d_head,
+                                  c.seq_len, self.table)),
+            ("attention", "attention", att_flop,
+             lambda: F.llama_attention(self.qkv, c.seq_len, c.n_heads, c.n_kv_heads, c.d_head, o=self.att.x)),
+            quant(self.att, "attention"),
+            lin("o", self.att, self.o),
+            ("residual+rmsnorm mlp", "glue", 4 * R * d + 4 * R * d,
+             lambda: F.llama_rmsnorm_quantise(self.o, self.g_mlp, LLAMA_EPS, res=self.H, h=self.h1, y=self.hn.x)),
+            quant(self.hn, "mlp input"),
+            lin("gate_up", self.hn, self.gu),
+            ("swiglu", "glue", 4 * R * ffn + 2 * R * ffn,
+             lambda: F.llama_swiglu_quantise(self.gu, ffn, a=self.act.x)),
+            quant(self.act, "down input"),
+            lin("down", self.act, self.down),
+            ("residual", "glue", 6 * R * d, lambda: F.llama_residual_add(self.h1, self.down, out=self.out)),
+        ]
+
     def run(self):
         for _, _, _, fn in self.calls:
             fn()
@@ -159,8 +230,9 @@ class DecoderLayer:
         return sum(w for _, k, w, _ in self.calls if k == "gemm_fwd")
 
     def biases(self) -> dict:
-        """Activation and weight biases (host ints; synchronises)."""
+        """Activation and weight biases (host ints; synchronises); with one
+        bias per sequence, the activation entries are lists."""
         b = {n: int(self.bw(n).item()) for n in self.w8t}
         for n, a in (("xn", self.xn), ("att", self.att), ("hn", self.hn), ("act", self.act)):
-            b[n] = int(a.bias.item())
+            b[n] = a.seg_bias.cpu().tolist() if self.bias_per == "sequence" else int(a.bias.item())
         return b

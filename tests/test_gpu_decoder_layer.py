@@ -156,3 +156,35 @@ def test_70b_layer_full_size_properties(gpu):
         layer.replay()
         torch.cuda.synchronize()
         assert torch.equal(layer.out, eager)
+
+
+@pytest.mark.parametrize("name", ["tiny-layer", "7b-layer-384"])
+def test_layer_per_sequence_biases_match_oracle(gpu, name):
+    """One activation bias per sequence (the per-data-sample biases of
+    App. D): segmented quantise + per-row-bias matmuls on the GPU against
+    the oracle chain with per-sequence quantisation; same bars."""
+    if name == "tiny-layer":
+        cfg = wl.LAYERS["tiny-layer"]
+    else:
+        full = wl.LAYERS["llama2-7b-layer"]
+        cfg = wl.LayerConfig("7b-layer-384", 8, "Llama-2-7B layer dims, 384 tokens", full.d_model, full.n_heads,
+                             full.n_kv_heads, full.d_head, full.ffn, 384, 256, full.w_std)
+    T = layer_inputs(cfg)
+    bits = {k: wl.bf16_bits(v) for k, v in T.items()}
+    p, _ = oracle_layer(cfg, T)
+    r = D.layer_forward(bits["H"], p, cfg.seq_len, cfg.n_heads, cfg.n_kv_heads, cfg.d_head, cfg.ffn,
+                        per_sequence=True)
+    W = {k: v.to(gpu) for k, v in T.items() if k != "H"}
+    layer = DL.DecoderLayer(cfg, W, gpu, bias_per="sequence")
+    layer.H.copy_(T["H"].to(gpu))
+    layer.run()
+    torch.cuda.synchronize()
+    compare(cfg, layer, p, r)
+    # graph replays match the eager call
+    eager = np_bits(layer.out).copy()
+    layer.capture()
+    for _ in range(2):
+        layer.out.zero_()
+        layer.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(np_bits(layer.out), eager)

@@ -281,3 +281,24 @@ def test_layer_forward_shapes_and_biases():
         assert m * 2.0 ** r[b] <= 448 < m * 2.0 ** (r[b] + 1)     # Eq. 3
     # the attention input at position 0 of each sequence is the unrotated projection
     assert np.array_equal(r["q"][0], r["qkv"][0, :nh * dh])
+
+
+def test_layer_forward_per_sequence_biases():
+    rng = np.random.default_rng(14)
+    d, nh, nkv, dh, ffn = 64, 4, 2, 16, 96
+    H = bits(rng.standard_normal((12, d)) * np.repeat([1.0, 40.0], 6)[:, None])   # two sequences, scales apart
+    p = _layer_params(rng, d, nh, nkv, dh, ffn)
+    # one sequence: the per-sequence mode is the per-tensor mode
+    a = D.layer_forward(H, p, seq_len=12, n_heads=nh, n_kv_heads=nkv, d_head=dh, ffn=ffn)
+    b = D.layer_forward(H, p, seq_len=12, n_heads=nh, n_kv_heads=nkv, d_head=dh, ffn=ffn, per_sequence=True)
+    assert np.array_equal(a["out"], b["out"])
+    assert [b["b_xn"], b["b_attn"], b["b_hn"], b["b_act"]] == [[a["b_xn"]], [a["b_attn"]], [a["b_hn"]], [a["b_act"]]]
+    # two sequences: Eq. 3 on each sequence's rows; the tensor's bias is the smallest of them
+    t = D.layer_forward(H, p, seq_len=6, n_heads=nh, n_kv_heads=nkv, d_head=dh, ffn=ffn)
+    s = D.layer_forward(H, p, seq_len=6, n_heads=nh, n_kv_heads=nkv, d_head=dh, ffn=ffn, per_sequence=True)
+    for x, bk in (("xn", "b_xn"), ("attn", "b_attn"), ("hn", "b_hn"), ("act", "b_act")):
+        assert len(s[bk]) == 2
+        for seg, bseg in zip((s[x][:6], s[x][6:]), s[bk]):
+            m = np.max(np.abs(vals(seg)))
+            assert m * 2.0 ** bseg <= 448 < m * 2.0 ** (bseg + 1)
+    assert min(s["b_xn"]) == t["b_xn"]          # same RMSNorm output in both modes
