@@ -150,3 +150,21 @@ def test_quantise_rejects_small_workspace(gpu):
     ws = torch.empty(8, dtype=torch.uint8, device=gpu)
     with pytest.raises(F.Fp8Error):
         F.fp8_quantise(x, F.E4M3, ws=ws)
+
+
+def test_quantise_workspace_reused(orc, gpu):
+    """One workspace across calls of different tensors and shapes (the steady
+    state of a step reuses one per tensor): every call matches the oracle,
+    whether its prediction is wrong (the first call, a new tensor) or right."""
+    from paper_2309_17224_amd import workloads as wl
+    ws = F.quantise_workspace(300, 1000, gpu)   # tiles of the largest shape
+    bias = torch.zeros(1, dtype=torch.int32, device=gpu)
+    for rows, cols, seed, std, fmt in ((300, 520, 1, 1.0, F.E4M3), (300, 520, 1, 1.0, F.E4M3),
+                                       (64, 64, 2, 3e-3, F.E5M2), (129, 1000, 3, 40.0, F.E4M3),
+                                       (129, 1000, 3, 40.0, F.E4M3)):
+        x = wl.small(rows, cols, std, seed)
+        ob, oa, ofl, oq, oqT = oracle_expect(orc, x, fmt)
+        q, qT, b, a, fl = F.fp8_quantise(x.to(gpu), fmt, 0, bias_pred=bias, bias=bias, want_qT=True, ws=ws)
+        torch.cuda.synchronize()
+        assert (i32(b), u32(a), u32(fl)) == (ob, oa, ofl)
+        assert np.array_equal(q.cpu().numpy(), oq) and np.array_equal(qT.cpu().numpy(), oqT)
