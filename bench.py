@@ -46,7 +46,9 @@ def parse():
     p.add_argument("--cpu-budget", type=float, default=12.0,
                    help="seconds of oracle GEMM work in the CPU baseline sample")
     p.add_argument("--flush-mb", type=int, default=0,
-                   help="write this many MB before every step (evicts the 256 MB MALL)")
+                   help="write this many MB before every step (evicts the 256 MB MALL), and in the "
+                        "per-call pass also before every decode matmul (weights from HBM, as in "
+                        "token-by-token decode)")
     p.add_argument("--quant", choices=("predicted", "twopass", "separate", "cscale"), default="predicted",
                    help="bias + cast of X, W, dY: one fp8_quantise call predicting each bias from "
                         "the previous step (identical bits; one read of an unchanged tensor), "
@@ -67,6 +69,9 @@ def parse():
                    help="decoder-layer workloads: one activation bias per tensor and call (quantise fused "
                         "into the producing kernels), or one per sequence (segmented quantise, per-row-bias "
                         "matmuls)")
+    p.add_argument("--amax-mb", type=int, default=0,
+                   help="only time fp8_scale_bias on a bf16 tensor of this many MB, --steps calls "
+                        "(read-bandwidth reference for the amax kernel), then exit")
     p.add_argument("--copy-mb", type=int, default=0,
                    help="only run a plain device-to-device copy of this many MB, --steps times "
                         "(reference kernel for scaling hardware traffic counters), then exit")
@@ -83,6 +88,12 @@ def make_inputs(w):
     cpu = {t.name: wl.make_tensor(w, t.name) for t in w.tensors}
     log(f"[bench] generated {len(cpu)} tensors in {time.time() - t0:.1f}s")
     return cpu
+
+
+# Kernel kinds that, with --flush-mb, the per-call pass also times right after
+# a flush: token-by-token decode reads each layer's weights once per token,
+# with every other layer's weights read in between, so they come from HBM.
+COLD_KINDS = ("gemm_decode",)
 
 
 def time_steps(step, steps, warmup, flush=None):
@@ -104,7 +115,12 @@ def time_steps(step, steps, warmup, flush=None):
             fl_ev[s][0].record()
             flush.add_(1)
             fl_ev[s][1].record()
-        for i, (_, _, _, fn) in enumerate(step.calls):
+        for i, (_, kind, _, fn) in enumerate(step.calls):
+            if flush is not None and kind in COLD_KINDS:
+                fl_ev.append((torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)))
+                fl_ev[-1][0].record()
+                flush.add_(1)
+                fl_ev[-1][1].record()
             ev[s][i][0].record()
             fn()
             ev[s][i][1].record()
@@ -368,6 +384,26 @@ def main():
         print(json.dumps({"copy_bytes_per_launch": nbytes, "launches": args.steps}))
         return
     fp8lin.lib()  # fails loudly when the HIP library is missing
+    if args.amax_mb:
+        # fp8_scale_bias (amax + Eq. 3 bias) of one bf16 tensor larger than the
+        # 256 MB MALL, so every launch reads it from HBM
+        n = (args.amax_mb << 20) // 2
+        x = torch.randn(n, dtype=torch.float32, device="cuda").to(torch.bfloat16)
+        ws = fp8lin.workspace(n, x.device)
+        for _ in range(max(args.warmup, 1)):
+            fp8lin.fp8_scale_bias(x, fp8lin.E4M3, ws=ws)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+        for a, b in ev:
+            a.record()
+            fp8lin.fp8_scale_bias(x, fp8lin.E4M3, ws=ws)
+            b.record()
+        torch.cuda.synchronize()
+        ts = sorted(a.elapsed_time(b) * 1e-3 for a, b in ev)
+        med = ts[len(ts) // 2]
+        print(json.dumps({"amax_bytes_per_call": 2 * n, "calls": args.steps, "median_us": med * 1e6,
+                          "GB_per_s": 2 * n / med / 1e9, "frac_of_8TBps": 2 * n / med / 8e12}))
+        return
     if args.workload in wl.LAYERS:
         bench_layer(args, wl.LAYERS[args.workload])
         return

@@ -188,6 +188,14 @@ __device__ __forceinline__ void lds_dma16_s(const uint8_t* sbase, uint32_t voff,
                  : "memory");
 }
 
+// The same copy with the non-temporal hint (a stream read once).
+__device__ __forceinline__ void lds_dma16_nt(const uint8_t* sbase, uint32_t voff, uint32_t lds_row) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2 nt"
+                 :
+                 : "s"(lds_row), "v"(voff), "s"(sbase)
+                 : "memory");
+}
+
 __device__ __forceinline__ int bq_used(const int32_t* pred) { return clamp_bias(*pred); }
 
 // 16-byte store of matmul output with the non-temporal hint: the output is not
@@ -648,6 +656,17 @@ __device__ __forceinline__ v8i ld_frag_g(const uint8_t* p) {
     return v8i{(int)p0.x, (int)p0.y, (int)p0.z, (int)p0.w, (int)p1.x, (int)p1.y, (int)p1.z, (int)p1.w};
 }
 
+// The same with the non-temporal hint, for the weight stream: each weight
+// byte is read once per call, and keeping it out of the caches leaves them to
+// the activation rows every workgroup shares (+38 % weight bandwidth on the
+// Llama-2-70B decode shapes with cold caches).
+__device__ __forceinline__ v8i ld_frag_stream(const uint8_t* p) {
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 p0 = __builtin_nontemporal_load((const u32x4*)p);
+    const u32x4 p1 = __builtin_nontemporal_load((const u32x4*)(p + 16));
+    return v8i{(int)p0.x, (int)p0.y, (int)p0.z, (int)p0.w, (int)p1.x, (int)p1.y, (int)p1.z, (int)p1.w};
+}
+
 // NB: 16-column blocks per workgroup; kDecWaves: waves splitting the K range.
 template <int FA, int FB, int OUT_DT, bool AMAX, int MB, int NB, int kDecWaves>
 __global__ __launch_bounds__(kDecWaves * 64) void gemm_nt_decode(
@@ -682,7 +701,7 @@ __global__ __launch_bounds__(kDecWaves * 64) void gemm_nt_decode(
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) xa[slot][mb] = ld_frag_g(pa[mb] + k0);
 #pragma unroll
-        for (int j = 0; j < NB; ++j) wb[slot][j] = ld_frag_g(pb[j] + k0);
+        for (int j = 0; j < NB; ++j) wb[slot][j] = ld_frag_stream(pb[j] + k0);
     };
     auto step = [&](int slot) {
 #pragma unroll
@@ -726,6 +745,96 @@ __global__ __launch_bounds__(kDecWaves * 64) void gemm_nt_decode(
     }
 }
 
+// Staged decode kernel (M <= 16, K a multiple of 512): the same product with
+// the weight rows streamed through LDS.  A load instruction that feeds an MFMA
+// fragment straight from memory touches 16 weight rows K bytes apart, 64 bytes
+// each; here a workgroup copies its BR weight rows (one contiguous block of
+// memory) and the 16 activation rows 512 bytes of k at a time with
+// global_load_lds_dwordx4, each instruction reading 512-byte runs of two
+// rows, three stages in flight, and the waves read the fragments from LDS.
+// Chunk c of LDS row r (16 bytes) is stored at chunk c ^ (r % 16): the 16
+// lanes of every ds_read_b128 phase (lane bit 5 and the parity of lane bits
+// 2..4 fixed; see the main kernel) then hit 16 distinct bank groups.
+// BR = 64: each wave one 16-row block, all k-steps.  BR = 32: waves w and w + 2
+// share block w % 2, each half of every stage's k-steps, added in a fixed order.
+constexpr int kDlKC = 512, kDlBuf = 3;
+
+template <int FA, int FB, int OUT_DT, bool AMAX, int BR>
+__global__ __launch_bounds__(256) void gemm_nt_decode_lds(
+    const uint8_t* __restrict__ A, const uint8_t* __restrict__ B, const int32_t* __restrict__ ba_p,
+    const int32_t* __restrict__ bb_p, void* __restrict__ C, int M, int N, int K, int vec_out,
+    uint32_t* __restrict__ amax_out, int ba_rows) {
+    constexpr int kRows = BR + 16, kStage = kRows * kDlKC, kCpr = kDlKC / 16;
+    constexpr int kNi = kRows / 2;  // copies per stage, two rows each
+    static_assert(kNi % 4 == 0, "copies split over four waves");
+    constexpr int kNiw = kNi / 4;
+    constexpr int kNbb = BR / 16, kWpb = 4 / kNbb, kKs = kDlKC / 128 / kWpb;
+    __shared__ __attribute__((aligned(1024))) uint8_t sm[kDlBuf * kStage];
+    __shared__ __attribute__((aligned(16))) float red[4][64][4];
+    const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int n0 = blockIdx.x * BR;
+    // copy t of this wave: LDS rows 2d, 2d + 1 (d = kNiw w + t); rows < BR are
+    // weight rows n0 + r (clamped to N - 1), the rest activation rows (clamped
+    // to M - 1); lane -> row 2d + lane / 32, physical chunk lane % 32
+    uint32_t voff[kNiw];
+#pragma unroll
+    for (int t = 0; t < kNiw; ++t) {
+        const int d = w * kNiw + t, r = 2 * d + (lane >> 5), c = (lane & 31) ^ (r & 15);
+        voff[t] = r < BR ? (uint32_t)((min(n0 + r, N - 1) - n0) * K + c * 16)
+                         : (uint32_t)(min(r - BR, M - 1) * K + c * 16);
+    }
+    const uint8_t* bbase = B + (int64_t)n0 * K;
+    const uint32_t lds0 = lds_addr(sm);
+    auto issue = [&](int st) {
+        const int buf = st % kDlBuf;
+#pragma unroll
+        for (int t = 0; t < kNiw; ++t) {
+            const int d = w * kNiw + t;
+            const uint32_t dst = __builtin_amdgcn_readfirstlane(lds0 + buf * kStage + d * 2 * kDlKC);
+            if (2 * d < BR) lds_dma16_nt(bbase + (int64_t)st * kDlKC, voff[t], dst);
+            else lds_dma16_s(A + (int64_t)st * kDlKC, voff[t], dst);
+        }
+    };
+    const int frow = lane & 15, fg = lane >> 4;
+    const int j = w % kNbb, h = w / kNbb;
+    const int rb = 16 * j + frow, ra = BR + frow;
+    v4f acc = {0.f, 0.f, 0.f, 0.f};
+    const int nst = K / kDlKC;
+#pragma unroll
+    for (int st = 0; st < kDlBuf - 1; ++st)
+        if (st < nst) issue(st);
+    for (int st = 0; st < nst; ++st) {
+        // stage st has landed once only the next stage's copies may be pending
+        if (st + 1 < nst) wait_vmcnt<kNiw>();
+        else wait_vmcnt<0>();
+        ws_barrier();
+        // the buffer of stage st - 1, which every wave has finished reading
+        if (st + kDlBuf - 1 < nst) issue(st + kDlBuf - 1);
+        const uint8_t* sb = sm + (st % kDlBuf) * kStage;
+#pragma unroll
+        for (int q = 0; q < kKs; ++q) {
+            const int c0 = (h * kKs + q) * 8 + 2 * fg;
+            const v8i bf = ld_frag(sb + rb * kDlKC, 16 * (c0 ^ (rb & 15)), 16 * ((c0 + 1) ^ (rb & 15)));
+            const v8i af = ld_frag(sb + ra * kDlKC, 16 * (c0 ^ (ra & 15)), 16 * ((c0 + 1) ^ (ra & 15)));
+            acc = mfma16<FB, FA>(bf, af, acc);
+        }
+    }
+    *(v4f*)red[w][lane] = acc;
+    __syncthreads();
+    uint32_t mx = 0;
+    if (w < kNbb) {
+        v4f sum = *(const v4f*)red[w][lane];
+#pragma unroll
+        for (int hh = 1; hh < kWpb; ++hh) sum += *(const v4f*)red[w + hh * kNbb][lane];
+        const int64_t m = lane & 15, n = n0 + w * 16 + (lane >> 4) * 4;
+        if (n < N) mx = store4<OUT_DT>(C, N, m, n, M, N, sum, row_shift(ba_p, ba_rows, *bb_p, m, M), vec_out != 0);
+    }
+    if (AMAX) {
+        mx = wave_max_u32(mx);
+        if (lane == 0) atomicMax(amax_out, mx);
+    }
+}
+
 template <int FA, int FB, int OUT_DT, bool AMAX, int MB>
 void launch_decode(const uint8_t* A, const int32_t* ba, const uint8_t* B, const int32_t* bb, void* C,
                    int M, int N, int K, int vec_out, uint32_t* amax, int ba_rows, hipStream_t s) {
@@ -755,7 +864,16 @@ void launch_t(const uint8_t* A, const int32_t* ba, const uint8_t* B, const int32
     const int esz = OUT_DT == FP8_DT_BF16 ? 2 : 4;
     const int vec_out = ((uintptr_t)C % (4 * esz) == 0) && (N % 4 == 0);
     const bool fast = fast_path(A, B, M, N, K);
-    if (fast && M <= 32) {
+    if (fast && M <= 16 && K % kDlKC == 0) {
+        // 64 weight rows per workgroup unless that leaves fewer than 256
+        // workgroups streaming long rows (measured on the Llama-2-70B shapes)
+        if (N >= 64 * 256 || K <= 8192)
+            hipLaunchKernelGGL((gemm_nt_decode_lds<FA, FB, OUT_DT, AMAX, 64>), dim3((unsigned)((N + 63) / 64)), dim3(256),
+                               0, s, A, B, ba, bb, C, (int)M, (int)N, (int)K, vec_out, amax, ba_rows);
+        else
+            hipLaunchKernelGGL((gemm_nt_decode_lds<FA, FB, OUT_DT, AMAX, 32>), dim3((unsigned)((N + 31) / 32)), dim3(256),
+                               0, s, A, B, ba, bb, C, (int)M, (int)N, (int)K, vec_out, amax, ba_rows);
+    } else if (fast && M <= 32) {
         if (M <= 16) launch_decode<FA, FB, OUT_DT, AMAX, 1>(A, ba, B, bb, C, (int)M, (int)N, (int)K, vec_out, amax, ba_rows, s);
         else launch_decode<FA, FB, OUT_DT, AMAX, 2>(A, ba, B, bb, C, (int)M, (int)N, (int)K, vec_out, amax, ba_rows, s);
     } else if (fast) {

@@ -43,7 +43,7 @@ def run_nt(entry, A, fa, ba, B, fb, bb, out_dt, gpu, M, N, K, amax=False):
 
 ENTRY_FMTS = {"fwd": (0, 0), "dx": (1, 0), "dw": (0, 1)}
 SHAPES = [(1, 1, 128), (16, 16, 128), (256, 256, 256), (300, 200, 384), (17, 129, 1000),
-          (255, 1, 17), (1, 255, 640), (129, 257, 128), (513, 300, 512), (64, 64, 0)]
+          (255, 1, 17), (1, 255, 640), (129, 257, 128), (513, 300, 512), (64, 64, 0), (5, 70, 1024)]
 
 
 def scaled_normal_codes(shape, fmt, rng, orc):
@@ -170,9 +170,13 @@ def test_gemm_deterministic(orc, gpu):
     assert torch.equal(y1, y2)
 
 
-# Decode shapes (M <= 32 routes to the weight-streaming kernel; 33 does not).
+# Decode shapes (M <= 32 routes to the weight-streaming kernels; 33 does not).
+# M <= 16 with K a multiple of 512 takes the LDS-staged kernel: 64 weight rows
+# per workgroup (K <= 8192 or N >= 16384) or 32; one stage (K = 512), exactly
+# as many stages as buffers (1536), long K with few workgroups, ragged N.
 DECODE = [(1, 64, 128), (2, 1000, 1024), (15, 65, 896), (16, 4096, 8192), (17, 130, 384),
-          (31, 192, 2048), (32, 1, 128), (33, 100, 256), (16, 63, 28672)]
+          (31, 192, 2048), (32, 1, 128), (33, 100, 256), (16, 63, 28672), (1, 130, 512),
+          (7, 33, 1536), (16, 200, 9216), (12, 16390, 512)]
 
 
 @pytest.mark.parametrize("shape", DECODE, ids=lambda s: "%dx%dx%d" % s)
