@@ -58,17 +58,23 @@ __global__ __launch_bounds__(kAmaxThreads) void amax_partial_kernel(const void* 
             uint4 v[kL];
 #pragma unroll
             for (int l = 0; l < kL; ++l) v[l] = ld_stream(p + i + l * kAmaxThreads);
+            // all kL loads issue before the first use (the scheduler would
+            // otherwise start folding the first one and wait for it alone)
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int l = 0; l < kL; ++l) fold(v[l]);
         }
-        // fewer than kL vectors of this lane left: zero is neutral for the maximum
-        {
+        // fewer than kL vectors of this lane left: unconditional loads of
+        // in-range vectors (a guarded load compiles to a branch and a wait per
+        // load), those past the range replaced by zero, neutral for the maximum
+        if (b1 > b0) {
             uint4 v[kL];
 #pragma unroll
-            for (int l = 0; l < kL; ++l) {
-                const int64_t j = i + l * kAmaxThreads;
-                v[l] = j < b1 ? ld_stream(p + j) : make_uint4(0u, 0u, 0u, 0u);
-            }
+            for (int l = 0; l < kL; ++l) v[l] = ld_stream(p + min(i + l * kAmaxThreads, b1 - 1));
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int l = 0; l < kL; ++l)
+                if (i + l * kAmaxThreads >= b1) v[l] = make_uint4(0u, 0u, 0u, 0u);
 #pragma unroll
             for (int l = 0; l < kL; ++l) fold(v[l]);
         }
@@ -88,8 +94,7 @@ __global__ __launch_bounds__(kAmaxThreads) void amax_finalize_kernel(
     const uint32_t* __restrict__ partial, int nparts, int32_t margin, int32_t* __restrict__ bias,
     uint32_t* __restrict__ amax_bits, uint32_t* __restrict__ flags) {
     __shared__ uint32_t red[kAmaxThreads / 64];
-    uint32_t m = 0;
-    for (int i = threadIdx.x; i < nparts; i += kAmaxThreads) m = max(m, partial[i]);
+    uint32_t m = strided_max<kAmaxThreads>(partial, nparts);
     m = block_max(m, red);
     if (threadIdx.x == 0) {
         const uint32_t a32 = DT == FP8_DT_BF16 ? (m << 16) : m;
@@ -307,8 +312,7 @@ __global__ __launch_bounds__(kCastThreads) void quant_pass2_kernel(
     __shared__ __attribute__((aligned(16))) uint8_t tile[kCastCols * kCastRows];
     __shared__ uint32_t red[kCastThreads / 64];
     __shared__ uint32_t amax_s;
-    uint32_t m = 0;
-    for (int i = threadIdx.x; i < nparts; i += kCastThreads) m = max(m, parts[i]);
+    uint32_t m = strided_max<kCastThreads>(parts, nparts);
     m = block_max(m, red);
     if (threadIdx.x == 0) amax_s = m;
     __syncthreads();

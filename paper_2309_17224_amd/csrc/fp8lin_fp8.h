@@ -96,6 +96,34 @@ __device__ __forceinline__ uint32_t block_max(uint32_t v, uint32_t* red) {
     return r;  // valid in thread 0
 }
 
+// Largest of p[threadIdx.x], p[threadIdx.x + NT], ... below n (this thread's
+// share of a block-wide maximum over n words), eight independent loads at a
+// time: a plain strided loop waits for each load before issuing the next.
+template <int NT>
+__device__ __forceinline__ uint32_t strided_max(const uint32_t* __restrict__ p, int n) {
+    uint32_t m = 0;
+    int i = threadIdx.x;
+    for (; i + 7 * NT < n; i += 8 * NT) {
+        uint32_t v[8];
+#pragma unroll
+        for (int l = 0; l < 8; ++l) v[l] = p[i + l * NT];
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int l = 0; l < 8; ++l) m = max(m, v[l]);
+    }
+    // the rest: unconditional loads of in-range words (a guarded load compiles
+    // to a branch and a wait per load), masked afterwards
+    if (n > 0) {
+        uint32_t v[8];
+#pragma unroll
+        for (int l = 0; l < 8; ++l) v[l] = p[min(i + l * NT, n - 1)];
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int l = 0; l < 8; ++l) m = max(m, i + l * NT < n ? v[l] : 0u);
+    }
+    return m;
+}
+
 __device__ __forceinline__ us2 fold_bf16(us2 m, uint4 v) {
     m = __builtin_elementwise_max(m, __builtin_bit_cast(us2, v.x & 0x7FFF7FFFu));
     m = __builtin_elementwise_max(m, __builtin_bit_cast(us2, v.y & 0x7FFF7FFFu));
