@@ -80,11 +80,12 @@ def test_special_values_per_segment(orc, gpu):
 
 
 @pytest.mark.parametrize("shape", [(300, 520, 384), (16, 1024, 256), (20, 512, 256), (100, 64, 100),
-                                   (2048, 1024, 512)], ids=str)
+                                   (2048, 1024, 512), (12, 1000, 1024), (9, 96, 10240)], ids=str)
 def test_fwd_rows_is_the_product_unscaled_per_row(gpu, shape):
     """Y of the per-row matmul is the same kernel's fp32 product S (taken with
     zero biases), unscaled row by row: Y[m] = round(S[m] * 2^-(rb[m] + bw)),
-    on the 256 x 256, decode and fallback kernels; and its epilogue amax."""
+    on the 256 x 256, decode (both staged row counts and the fragment-loading
+    kernel) and fallback kernels; and its epilogue amax."""
     M, N, K = shape
     x = data(M, K, M + K, F.DT_BF16).to(gpu)
     g = torch.Generator().manual_seed(N)
@@ -118,8 +119,8 @@ def test_fwd_rows_against_oracle_on_exact_products(orc, gpu):
         v = vals[rng.integers(0, len(vals), size=(r, c))]
         return (v | (rng.integers(0, 2, size=(r, c)).astype(np.uint8) << 7) * (v != 0)).astype(np.uint8)
 
-    for M in (300, 20):
-        N, K = 512, 256
+    for M, K in ((300, 256), (20, 256), (12, 512)):
+        N = 512
         x8, w8t = codes(M, K), codes(N, K)
         rows_b = (np.arange(M) % 9 - 4).astype(np.int32)
         yref = orc.gemm_nt_rows(x8, 0, rows_b, w8t, 0, 1, out_dt=orc.BF16)
