@@ -250,58 +250,73 @@ __device__ __forceinline__ int32_t bias_of_fmt(int fmt, uint32_t a, int32_t marg
     }
 }
 
-template <int FA, int FB, int OUT_DT, bool AMAX, int QF = -1>
-__global__ __launch_bounds__(kMainThreads) void gemm_nt_256(
-    const uint8_t* __restrict__ A, const uint8_t* __restrict__ B, const int32_t* __restrict__ ba_p,
-    const int32_t* __restrict__ bb_p, void* __restrict__ C, int M, int N, int K, int tiles_m,
-    int tiles_n, int vec_out, uint32_t* __restrict__ amax_out, QuantOut qo, BiasOut bo, int ba_rows) {
+// One output tile of 256 rows x TN columns (TN = 64..256; each wave owns 64
+// rows x TN/2 columns), tile number bid of nb in this workgroup's share of the
+// launch, over columns [col0, col0 + tiles_n TN) of C.  The last workgroup of
+// the launch takes the bias when bo.ws is set.
+template <int FA, int FB, int OUT_DT, bool AMAX, int QF, int TN>
+__device__ __forceinline__ void gemm_tile(
+    uint8_t* __restrict__ smem, int bid, int nb, const uint8_t* __restrict__ A, const uint8_t* __restrict__ B,
+    const int32_t* __restrict__ ba_p, const int32_t* __restrict__ bb_p, void* __restrict__ C, int M, int N, int K,
+    int tiles_m, int tiles_n, int col0, int vec_out, uint32_t* __restrict__ amax_out, const QuantOut& qo,
+    const BiasOut& bo, int ba_rows) {
     static_assert(QF < 0 || OUT_DT == FP8_DT_BF16, "fused quantise is for bf16 outputs");
-    __shared__ __attribute__((aligned(1024))) uint8_t smem[kSmemBytes];
+    static_assert(QF < 0 || TN == 256, "fused quantise stages whole 256 x 256 tiles");
+    static_assert(TN % 64 == 0 && TN >= 64 && TN <= 256, "tile width");
+    constexpr int kNbw = TN / 32;                  // 16-column blocks per wave, B copies per loader wave
+    constexpr int kStage = kTileBytes + TN * kBK;  // A tile + B tile
+    constexpr int kNf = 4 + kNbw;                  // fragment pieces a wave reads per step
+    constexpr int kNc = 8 + kNbw;                  // copies a loader wave issues per stage
 
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     // group (0: waves 0-3, 1: waves 4-7) and quadrant; wave-uniform
     const int g = __builtin_amdgcn_readfirstlane(w >> 2), sq = __builtin_amdgcn_readfirstlane(w & 3);
     int tm, tn;
-    tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
-    const int m0 = tm * kBM, n0 = tn * kBN;
+    tile_of(bid, nb, tiles_m, tiles_n, tm, tn);
+    const int m0 = tm * kBM, n0 = col0 + tn * TN;
 
-    // Loader (group 0): wave sq fills rows [64 sq, 64 sq + 64) of both tiles,
-    // 8 rows per copy (voff[0..7] for A, voff[8..15] for B); lane -> row r =
-    // 64 sq + 8 i + lane / 8 and physical chunk lane % 8, which holds logical
-    // chunk (lane % 8) ^ chunk_swz(r).  Rows past the matrix edge re-read the
-    // last row (their outputs are not stored).  Offsets are relative to the
-    // tile's first row, so they fit 32 bits for K < 2^22.
+    // Loader (group 0): wave sq fills rows [64 sq, 64 sq + 64) of the A tile
+    // and [TN/4 sq, TN/4 (sq + 1)) of the B tile, 8 rows per copy (voff[0..7]
+    // for A, voff[8..] for B); lane -> row r = (first row) + 8 i + lane / 8 and
+    // physical chunk lane % 8, which holds logical chunk (lane % 8) ^
+    // chunk_swz(r).  Rows past the matrix edge re-read the last row (their
+    // outputs are not stored).  Offsets are relative to the tile's first row,
+    // so they fit 32 bits for K < 2^22.
     const int lrow = lane >> 3;
-    uint32_t voff[16];
+    uint32_t voff[kNc];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         const int r = sq * 64 + i * 8 + lrow;
-        const int lchunk = (lane & 7) ^ chunk_swz(r);
-        voff[i] = (uint32_t)((min(m0 + r, M - 1) - m0) * K + lchunk * 16);
-        voff[8 + i] = (uint32_t)((min(n0 + r, N - 1) - n0) * K + lchunk * 16);
+        voff[i] = (uint32_t)((min(m0 + r, M - 1) - m0) * K + ((lane & 7) ^ chunk_swz(r)) * 16);
+    }
+#pragma unroll
+    for (int i = 0; i < kNbw; ++i) {
+        const int r = sq * (TN / 4) + i * 8 + lrow;
+        voff[8 + i] = (uint32_t)((min(n0 + r, N - 1) - n0) * K + ((lane & 7) ^ chunk_swz(r)) * 16);
     }
     const uint8_t* baseA = A + (int64_t)m0 * K;
     const uint8_t* baseB = B + (int64_t)n0 * K;
-    // LDS address of this wave's first loader row (wave-uniform); copy d of
-    // 16 goes to operand d / 8, row group d % 8.
-    const uint32_t lds_w = __builtin_amdgcn_readfirstlane(lds_addr(smem) + sq * 64 * kBK);
+    // LDS addresses of this wave's first loader rows (wave-uniform); copy d
+    // < 8 fills A row group d, copy d >= 8 B row group d - 8.
+    const uint32_t lds_a = __builtin_amdgcn_readfirstlane(lds_addr(smem) + sq * 64 * kBK);
+    const uint32_t lds_b = __builtin_amdgcn_readfirstlane(lds_addr(smem) + kTileBytes + sq * (TN / 4) * kBK);
     auto dma = [&](int d, int stage, int k0) {
         lds_dma16_s((d >= 8 ? baseB : baseA) + k0, voff[d],
-                    lds_w + stage * 2 * kTileBytes + (d >= 8 ? kTileBytes : 0) + (d & 7) * 8 * kBK);
+                    (d >= 8 ? lds_b + (d - 8) * 8 * kBK : lds_a + d * 8 * kBK) + stage * kStage);
     };
 
-    // this wave's sub-tile: rows [wr0, wr0 + 64), columns [wc0, wc0 + 128) of the tile
-    const int wr0 = (sq >> 1) * 128 + g * 64, wc0 = (sq & 1) * 128;
+    // this wave's sub-tile: rows [wr0, wr0 + 64), columns [wc0, wc0 + TN/2) of the tile
+    const int wr0 = (sq >> 1) * 128 + g * 64, wc0 = (sq & 1) * (TN / 2);
     const int frow = lane & 15, fg = lane >> 4;
     // byte offsets (within a 16-row block) of this lane's two fragment pieces
     const int fo0 = frow * kBK + (((2 * fg) ^ chunk_swz(frow)) << 4);
     const int fo1 = frow * kBK + (((2 * fg + 1) ^ chunk_swz(frow)) << 4);
 
-    v4f acc[4][8];
+    v4f acc[4][kNbw];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < kNbw; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
     // Ping-pong pipeline.  Phases are separated by workgroup barriers; in
     // every phase one group issues MFMAs and the other loads:
@@ -319,11 +334,11 @@ __global__ __launch_bounds__(kMainThreads) void gemm_nt_256(
     const int nk = K / kBK;
     if (g == 0 && nk > 0) {
 #pragma unroll
-        for (int d = 0; d < 16; ++d) dma(d, 0, 0);
+        for (int d = 0; d < kNc; ++d) dma(d, 0, 0);
         if (nk > 1) {
 #pragma unroll
-            for (int d = 0; d < 16; ++d) dma(d, 1, kBK);
-            wait_vmcnt<16>();
+            for (int d = 0; d < kNc; ++d) dma(d, 1, kBK);
+            wait_vmcnt<kNc>();
         } else {
             wait_vmcnt<0>();
         }
@@ -332,22 +347,23 @@ __global__ __launch_bounds__(kMainThreads) void gemm_nt_256(
         ws_barrier();
         if (g == 1) ws_barrier();
     }
-    v8i af[4], bf[8];
+    v8i af[4], bf[kNbw];
     for (int kt = 0; kt < nk; ++kt) {
-        const uint8_t* sa = smem + (kt & 1) * 2 * kTileBytes + wr0 * kBK;
-        const uint8_t* sb = smem + (kt & 1) * 2 * kTileBytes + kTileBytes + wc0 * kBK;
+        const uint8_t* sa = smem + (kt & 1) * kStage + wr0 * kBK;
+        const uint8_t* sb = smem + (kt & 1) * kStage + kTileBytes + wc0 * kBK;
         if (g == 0 && kt >= 1 && kt + 1 < nk) {
             const int st = (kt + 1) & 1, k1 = (kt + 1) * kBK;
+            // kNc = kNf + 4 copies spread over the kNf fragment reads
 #pragma unroll
-            for (int q = 0; q < 12; ++q) {
+            for (int q = 0; q < kNf; ++q) {
                 if (q < 4) af[q] = ld_frag(sa + q * 16 * kBK, fo0, fo1);
                 else bf[q - 4] = ld_frag(sb + (q - 4) * 16 * kBK, fo0, fo1);
                 dma(q, st, k1);
-                if (q < 4) dma(12 + q, st, k1);
+                if (q < 4) dma(kNf + q, st, k1);
             }
         } else {
 #pragma unroll
-            for (int q = 0; q < 12; ++q) {
+            for (int q = 0; q < kNf; ++q) {
                 if (q < 4) af[q] = ld_frag(sa + q * 16 * kBK, fo0, fo1);
                 else bf[q - 4] = ld_frag(sb + (q - 4) * 16 * kBK, fo0, fo1);
             }
@@ -357,7 +373,7 @@ __global__ __launch_bounds__(kMainThreads) void gemm_nt_256(
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
+            for (int j = 0; j < kNbw; ++j) {
                 acc[i][j] = mfma16<FB, FA>(bf[j], af[i], acc[i][j]);
                 __builtin_amdgcn_sched_barrier(0);
             }
@@ -398,7 +414,7 @@ __global__ __launch_bounds__(kMainThreads) void gemm_nt_256(
             for (int ii = 0; ii < 2; ++ii) {
                 const int i = 2 * i2 + ii;
 #pragma unroll
-                for (int j = 0; j < 8; ++j) {
+                for (int j = 0; j < kNbw; ++j) {
                     const uint32_t lo = pack_bf16x2(ldexpf(acc[i][j][0], shr[i]), ldexpf(acc[i][j][1], shr[i]));
                     const uint32_t hi = pack_bf16x2(ldexpf(acc[i][j][2], shr[i]), ldexpf(acc[i][j][3], shr[i]));
                     if (AMAX || QF >= 0) {
@@ -423,7 +439,7 @@ __global__ __launch_bounds__(kMainThreads) void gemm_nt_256(
                 const int row = 4 * t + prow, c16 = lane & 15;
                 const uint4 v = *(const uint4*)(ep + row * kEpRowBf16 + c16 * 16);
                 const int64_t m = m0 + wr0 + i2 * 32 + row, n = n0 + wc0 + c16 * 8;
-                if (m < M) {
+                if (m < M && c16 < TN / 16) {
                     uint16_t* p = (uint16_t*)C + m * N + n;
                     if (vec_out && n + 8 <= N) {
                         st_stream(p, v);
@@ -494,7 +510,7 @@ __global__ __launch_bounds__(kMainThreads) void gemm_nt_256(
             for (int ii = 0; ii < 2; ++ii) {
                 const int i = 2 * i2 + ii;
 #pragma unroll
-                for (int j = 0; j < 8; ++j) {
+                for (int j = 0; j < kNbw; ++j) {
                     float y[4];
 #pragma unroll
                     for (int v = 0; v < 4; ++v) {
@@ -510,7 +526,7 @@ __global__ __launch_bounds__(kMainThreads) void gemm_nt_256(
                 const int row = 2 * t + (lane >> 5), c32 = lane & 31;
                 const float4 v = *(const float4*)(ep + row * kEpRowF32 + c32 * 16);
                 const int64_t m = m0 + wr0 + i2 * 32 + row, n = n0 + wc0 + c32 * 4;
-                if (m < M) {
+                if (m < M && c32 < TN / 8) {
                     float* p = (float*)C + m * N + n;
                     if (vec_out && n + 4 <= N) {
                         st_stream(p, make_uint4(__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)));
@@ -559,6 +575,29 @@ __global__ __launch_bounds__(kMainThreads) void gemm_nt_256(
             }
         }
     }
+}
+
+// The 256-row kernel.  Workgroups below g1 take 256 x 256 tiles (tiles_m x
+// tiles_n of them); with TN2 > 0 the rest take tiles TN2 wide over the
+// columns after them (tiles_m x tiles_n2), a last round of narrower tiles
+// instead of a partial round of full ones (see narrow_split).  g1 is a whole
+// number of rounds of 8 workgroups per XCD, so both parts keep their XCD
+// layout.
+template <int FA, int FB, int OUT_DT, bool AMAX, int QF = -1, int TN2 = 0>
+__global__ __launch_bounds__(kMainThreads) void gemm_nt_256(
+    const uint8_t* __restrict__ A, const uint8_t* __restrict__ B, const int32_t* __restrict__ ba_p,
+    const int32_t* __restrict__ bb_p, void* __restrict__ C, int M, int N, int K, int tiles_m,
+    int tiles_n, int vec_out, uint32_t* __restrict__ amax_out, QuantOut qo, BiasOut bo, int ba_rows,
+    int g1, int tiles_n2) {
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[kSmemBytes];
+    const int b = blockIdx.x;
+    if (TN2 == 0 || b < g1)
+        gemm_tile<FA, FB, OUT_DT, AMAX, QF, 256>(smem, b, TN2 == 0 ? (int)gridDim.x : g1, A, B, ba_p, bb_p, C, M, N,
+                                                 K, tiles_m, tiles_n, 0, vec_out, amax_out, qo, bo, ba_rows);
+    else
+        gemm_tile<FA, FB, OUT_DT, AMAX, -1, (TN2 > 0 ? TN2 : 256)>(smem, b - g1, (int)gridDim.x - g1, A, B, ba_p,
+                                                                   bb_p, C, M, N, K, tiles_m, tiles_n2, tiles_n * kBN,
+                                                                   vec_out, amax_out, qo, bo, ba_rows);
 }
 
 // ------------------------------------------------------------ fallback kernel
@@ -857,7 +896,44 @@ bool fast_path(const uint8_t* A, const uint8_t* B, int64_t M, int64_t N, int64_t
            N <= INT32_MAX && K < (1 << 22);
 }
 
-// bo.ws != nullptr only where the 256 x 256 kernel runs (fast_path, M > 32).
+// Workgroups of the 256-row kernel that run at once (one per CU of gfx950).
+constexpr int kRound = 256;
+
+// Columns of 256-wide tiles taken in whole rounds of kRound workgroups, and
+// the rest in one round of narrower tiles: with all 256-wide, a last partial
+// round costs as much as a full one.  E.g. 4096 x 11008 (16 x 43 tiles):
+// two rounds over the first 8192 columns, then 240 tiles 192 wide (0.75 of
+// the work each) over the last 2816.  Every output is still computed by one
+// workgroup over the whole K in the same order, so the bits do not change.
+// ndp: 256-wide tile columns; tw, tn2: width and count of the narrow ones
+// (tw = 0: no narrow launch).
+void narrow_split(int tiles_m, int tiles_n, int64_t N, int& ndp, int& tw, int& tn2) {
+    ndp = tiles_n;
+    tw = 0;
+    tn2 = 0;
+    const int64_t T = (int64_t)tiles_m * tiles_n;
+    if (T % kRound == 0 || tiles_m > kRound) return;
+    int gcd = kRound, b = tiles_m;
+    while (b) {
+        const int t = gcd % b;
+        gcd = b;
+        b = t;
+    }
+    const int step = kRound / gcd;  // tile columns per whole number of rounds
+    const int c = tiles_n / step * step;
+    const int64_t nrem = N - (int64_t)c * kBN;
+    for (int w : {64, 128, 192}) {
+        const int64_t strips = (nrem + w - 1) / w;
+        if (tiles_m * strips <= kRound) {
+            ndp = c;
+            tw = w;
+            tn2 = (int)strips;
+            return;
+        }
+    }
+}
+
+// bo.ws != nullptr only where the 256-row kernel runs (fast_path, M > 32).
 template <int FA, int FB, int OUT_DT, bool AMAX>
 void launch_t(const uint8_t* A, const int32_t* ba, const uint8_t* B, const int32_t* bb, void* C,
               int64_t M, int64_t N, int64_t K, uint32_t* amax, const BiasOut& bo, int ba_rows, hipStream_t s) {
@@ -879,8 +955,17 @@ void launch_t(const uint8_t* A, const int32_t* ba, const uint8_t* B, const int32
     } else if (fast) {
         const int tiles_m = (int)((M + kBM - 1) / kBM), tiles_n = (int)((N + kBN - 1) / kBN);
         const int vec16 = ((uintptr_t)C % 16 == 0) && ((N * esz) % 16 == 0);
-        hipLaunchKernelGGL((gemm_nt_256<FA, FB, OUT_DT, AMAX>), dim3(tiles_m * tiles_n), dim3(kMainThreads), 0,
-                           s, A, B, ba, bb, C, (int)M, (int)N, (int)K, tiles_m, tiles_n, vec16, amax, QuantOut{}, bo, ba_rows);
+        int ndp, tw, tn2;
+        narrow_split(tiles_m, tiles_n, N, ndp, tw, tn2);
+        const int g1 = tiles_m * ndp, grid = g1 + tiles_m * tn2;
+#define FP8LIN_GEMM256(TW)                                                                                         \
+    hipLaunchKernelGGL((gemm_nt_256<FA, FB, OUT_DT, AMAX, -1, TW>), dim3(grid), dim3(kMainThreads), 0, s, A, B, ba, \
+                       bb, C, (int)M, (int)N, (int)K, tiles_m, ndp, vec16, amax, QuantOut{}, bo, ba_rows, g1, tn2)
+        if (tw == 64) FP8LIN_GEMM256(64);
+        else if (tw == 128) FP8LIN_GEMM256(128);
+        else if (tw == 192) FP8LIN_GEMM256(192);
+        else FP8LIN_GEMM256(0);
+#undef FP8LIN_GEMM256
     } else {
         const int64_t tiles_m = (M + kSBM - 1) / kSBM, tiles_n = (N + kSBN - 1) / kSBN;
         hipLaunchKernelGGL((gemm_nt_small<FA, FB, OUT_DT, AMAX>), dim3((unsigned)(tiles_m * tiles_n)),
@@ -921,7 +1006,8 @@ void launch_fused_t(const uint8_t* A, const int32_t* ba, const uint8_t* B, const
     const int tiles_m = (int)((M + kBM - 1) / kBM), tiles_n = (int)((N + kBN - 1) / kBN);
     const int vec16 = ((uintptr_t)C % 16 == 0) && ((N * 2) % 16 == 0);
     hipLaunchKernelGGL((gemm_nt_256<FA, FB, FP8_DT_BF16, false, QF>), dim3(tiles_m * tiles_n), dim3(kMainThreads), 0,
-                       s, A, B, ba, bb, C, (int)M, (int)N, (int)K, tiles_m, tiles_n, vec16, nullptr, qo, BiasOut{}, 0);
+                       s, A, B, ba, bb, C, (int)M, (int)N, (int)K, tiles_m, tiles_n, vec16, nullptr, qo, BiasOut{}, 0,
+                       tiles_m * tiles_n, 0);
 }
 
 template <int FA, int FB>
