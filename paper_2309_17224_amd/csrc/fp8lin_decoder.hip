@@ -284,6 +284,22 @@ __device__ __forceinline__ f4_t mfma_bf16(u32x4 a, u32x4 b, f4_t c) {
 
 __device__ __forceinline__ u32x4 ldg16(const uint16_t* p) { return *(const u32x4*)p; }
 
+// 32-bit LDS address of a pointer into a __shared__ array.
+__device__ __forceinline__ uint32_t lds_addr32(const void* p) {
+    return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
+}
+
+// Direct global -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4 with
+// a wave-uniform 64-bit base and a 32-bit lane byte offset): lane i's bytes
+// land at lds_dst + 16 i.  Issued from inline assembly, so the compiler does
+// not track it: the caller waits (s_waitcnt vmcnt) before the data is read.
+__device__ __forceinline__ void lds_copy16(const void* sbase, uint32_t voff, uint32_t lds_dst) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+                 :
+                 : "s"(lds_dst), "v"(voff), "s"(sbase)
+                 : "memory");
+}
+
 // Maximum / sum over lanes l, l ^ 16, l ^ 32, l ^ 48 (the four lanes that hold
 // one query's scores) with VALU lane swaps: swapping a value with itself
 // between rows 0-1 and 2-3 of 16 lanes (then between the two halves of the
@@ -350,32 +366,47 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
         for (int ds = 0; ds < 4; ++ds) qf[qt][ds] = ldg16(Qg + (int64_t)row * p.ld + 32 * ds + 8 * g);
     }
 
-    // Staging roles: K as four 16-byte chunks per lane (key idx/16, chunk
-    // idx%16); V as keys 4u .. 4u+3 x columns 8v .. 8v+7 (u = tid/16, v = tid%16).
+    // Staging roles: K goes straight to LDS, wave w copying keys 16 w .. 16 w + 15
+    // (4 copies of 4 rows; lane l: key 16 w + 4 j + l/16, physical chunk l%16,
+    // which holds logical chunk (l%16) ^ (key mod 16)); V goes through
+    // registers, keys 4u .. 4u+3 x columns 8v .. 8v+7 (u = tid/16, v = tid%16).
     // Rows past kend read row kend-1 (a finite copy; those keys are masked).
-    // Full blocks: a wave-uniform block base plus per-lane 32-bit offsets
-    // (rows tid/16 + 16 j of K, 4 (tid/16) + j of V); the last, partial block
-    // clamps each row.
+    // Full blocks: a wave-uniform block base plus per-lane 32-bit offsets; the
+    // last, partial block clamps each row.
     const int vu = w + 4 * ((tid >> 4) & 3), vv = tid & 15;
     const int ld = (int)p.ld;
-    const int koff = (tid >> 4) * ld + (tid & 15) * 8, voff = 4 * vu * ld + 8 * vv;
-    u32x4 kreg[4], vreg[4];
-    auto load_block = [&](int kb) {
+    const int voff = 4 * vu * ld + 8 * vv;
+    const int wu = __builtin_amdgcn_readfirstlane(w);
+    int kkey[4];
+    uint32_t kboff[4];  // byte offsets of this lane's K copies in a full block
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        kkey[j] = 16 * wu + 4 * j + (lane >> 4);
+        kboff[j] = (uint32_t)(kkey[j] * ld + 8 * ((lane & 15) ^ (kkey[j] & 15))) * 2u;
+    }
+    u32x4 vreg[4];
+    auto copy_k = [&](int kb, int buf) {
         const int kbase = kb * kBk;
         const uint16_t* kp = Kg + (int64_t)kbase * p.ld;
-        const uint16_t* vp = Vg + (int64_t)kbase * p.ld;
+        const uint32_t dst = lds_addr32(lds + buf * 2 * kKvBytes) + (16 * wu) * 256;
         if (kbase + kBk <= kend) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) kreg[j] = ldg16(kp + koff + 16 * j * ld);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) vreg[j] = ldg16(vp + voff + j * ld);
+            for (int j = 0; j < 4; ++j) lds_copy16(kp, kboff[j], dst + j * 1024);
         } else {
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const int idx = tid + kThreads * j;
-                const int row = min(kbase + (idx >> 4), kend - 1) - kbase;
-                kreg[j] = ldg16(kp + row * ld + (idx & 15) * 8);
+                const int row = min(kbase + kkey[j], kend - 1) - kbase;
+                lds_copy16(kp, (uint32_t)(row * ld + 8 * ((lane & 15) ^ (kkey[j] & 15))) * 2u, dst + j * 1024);
             }
+        }
+    };
+    auto load_v = [&](int kb) {
+        const int kbase = kb * kBk;
+        const uint16_t* vp = Vg + (int64_t)kbase * p.ld;
+        if (kbase + kBk <= kend) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) vreg[j] = ldg16(vp + voff + j * ld);
+        } else {
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int row = min(kbase + 4 * vu + j, kend - 1) - kbase;
@@ -391,15 +422,8 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
     // a slice (vu = wave + 4 (lane / 16)), every 8-byte write instruction
     // spreads evenly over the 64 banks and every fragment read is
     // conflict-free (checked against the measured ds_read_b128 phases).
-    auto store_block = [&](int buf) {
-        uint8_t* Kl = lds + buf * 2 * kKvBytes;
-        uint8_t* Vl = Kl + kKvBytes;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int idx = tid + kThreads * j;
-            const int key = idx >> 4, c = idx & 15;
-            *(u32x4*)(Kl + key * 256 + ((c ^ (key & 15)) << 4)) = kreg[j];
-        }
+    auto store_v = [&](int buf) {
+        uint8_t* Vl = lds + buf * 2 * kKvBytes + kKvBytes;
         const int kp = 32 * (vu >> 3) + 8 * (vu & 3) + 4 * ((vu >> 2) & 1);  // permuted position of key 4u
         const int cb = kp >> 3, ob = (kp & 7) * 2;
 #pragma unroll
@@ -422,10 +446,12 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
     const float c2 = p.scale_log2;
     const float lazy = 8.0f / c2;  // 2^8 in probability, in units of raw scores
 
-    load_block(0);
-    store_block(0);
-    // Every load of the prologue (the query fragments included) has landed:
-    // the loop's waits then only cover the loads issued inside the loop.
+    copy_k(0, 0);
+    load_v(0);
+    store_v(0);
+    // Every load of the prologue (the query fragments and the K copies
+    // included) has landed: the loop's waits then only cover the loads issued
+    // inside the loop.
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     for (int kb = 0; kb < nkb; ++kb) {
@@ -434,7 +460,8 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
         // its own block into the other buffer, which nothing reads): a load
         // that could reach the back-edge unconsumed would make the compiler
         // wait for these loads in the middle of the matrix work.
-        load_block(kb + 1 < nkb ? kb + 1 : kb);
+        copy_k(kb + 1 < nkb ? kb + 1 : kb, buf ^ 1);
+        load_v(kb + 1 < nkb ? kb + 1 : kb);
         const int kbase = kb * kBk;
         // Every wave runs every block: one entirely above a wave's diagonal
         // (at most 2 of 4 waves, in the last block) is masked to zero weight,
@@ -523,7 +550,10 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
                 }
             }
         }
-        store_block(buf ^ 1);
+        store_v(buf ^ 1);
+        // this wave's K copies into the other buffer (not tracked by the
+        // compiler) have landed before the barrier
+        __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
     }
 
