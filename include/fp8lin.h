@@ -184,6 +184,36 @@ int32_t fp8_quantise(const void *x, int32_t dt, int64_t rows, int64_t cols, int6
                      uint8_t *qT, int64_t ldqT, void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * fp8_quantise_batch -- fp8_quantise of n tensors (1 <= n <=
+ * FP8_QUANTISE_BATCH_MAX) of one element type dt and format fmt, with one
+ * margin, in two launches instead of 2 n: the same outputs, bit for bit, as n
+ * separate fp8_quantise calls in order.  Meant for tensors that are ready at
+ * the same time (a linear's weight and input before its forward matmul).
+ * t[i]: the arguments of call i (host array, read before returning; every
+ * pointer in it is a device pointer).  Either every non-empty tensor has a
+ * bias_pred or none has.  Workspaces must be distinct, and no output may
+ * alias another tensor's input or outputs.  n == 0 does nothing.
+ * Errors: those fp8_quantise would return for any t[i], FP8_EINVAL for n out
+ * of range, a null t or mixed predictions; nothing is launched then.
+ */
+#define FP8_QUANTISE_BATCH_MAX 4
+typedef struct fp8_quantise_args {
+    const void *x;
+    int64_t rows, cols, ldx;
+    const int32_t *bias_pred;
+    int32_t *bias;
+    uint32_t *amax_bits, *flags;
+    uint8_t *q;
+    int64_t ldq;
+    uint8_t *qT;
+    int64_t ldqT;
+    void *ws;
+    size_t ws_bytes;
+} fp8_quantise_args;
+int32_t fp8_quantise_batch(int32_t n, const fp8_quantise_args *t, int32_t dt, int32_t fmt,
+                           int32_t margin, void *stream);
+
+/*
  * fp8_quantise_segments -- FP8-AMAX for every row segment of one tensor in one
  * call: the paper takes a bias per micro-batch and per data or tensor replica
  * (Sec. 4), and per data sample at inference (the per-sample activation biases

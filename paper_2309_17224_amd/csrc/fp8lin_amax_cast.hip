@@ -302,6 +302,34 @@ __global__ __launch_bounds__(kCastThreads) void quant_pass1_kernel(
     if (threadIdx.x == 0) parts[blockIdx.x] = bm;
 }
 
+// Pass 2 of one tensor as workgroup bid of nb: see quant_pass2_kernel.
+template <int DT, int FMT>
+__device__ __forceinline__ void quant_pass2_body(
+    int bid, int nb, uint8_t* tile, uint32_t* red, uint32_t& amax_s, const void* __restrict__ x,
+    int64_t rows, int64_t cols, int64_t ldx, const uint32_t* __restrict__ parts, int nparts,
+    const int32_t* __restrict__ used, int have_used, int32_t margin, int32_t* __restrict__ bias,
+    uint32_t* __restrict__ amax_bits, uint32_t* __restrict__ flags, uint8_t* __restrict__ q, int64_t ldq,
+    uint8_t* __restrict__ qT, int64_t ldqT, int64_t tiles_c, int64_t ncast, int vec_in, int vec_q,
+    int vec_qT) {
+    uint32_t m = strided_max<kCastThreads>(parts, nparts);
+    m = block_max(m, red);
+    if (threadIdx.x == 0) amax_s = m;
+    __syncthreads();
+    const uint32_t a32 = DT == FP8_DT_BF16 ? (amax_s << 16) : amax_s;
+    uint32_t fl;
+    const int32_t bx = bias_of<FMT>(a32, margin, &fl);
+    if (bid == 0 && threadIdx.x == 0) {
+        *bias = bx;
+        if (amax_bits) *amax_bits = a32;
+        if (flags) *flags = fl;
+    }
+    const int b = clamp_bias(bx);
+    if (have_used && *used == b) return;  // pass 1 already wrote these codes
+    for (int64_t t = bid; t < ncast; t += nb)
+        cast_tile<DT, FMT, false>(x, rows, cols, ldx, b, q, ldq, qT, ldqT, t / tiles_c, t % tiles_c,
+                                  vec_in, vec_q, vec_qT, tile);
+}
+
 template <int DT, int FMT>
 __global__ __launch_bounds__(kCastThreads) void quant_pass2_kernel(
     const void* __restrict__ x, int64_t rows, int64_t cols, int64_t ldx,
@@ -312,23 +340,70 @@ __global__ __launch_bounds__(kCastThreads) void quant_pass2_kernel(
     __shared__ __attribute__((aligned(16))) uint8_t tile[kCastCols * kCastRows];
     __shared__ uint32_t red[kCastThreads / 64];
     __shared__ uint32_t amax_s;
-    uint32_t m = strided_max<kCastThreads>(parts, nparts);
-    m = block_max(m, red);
-    if (threadIdx.x == 0) amax_s = m;
-    __syncthreads();
-    const uint32_t a32 = DT == FP8_DT_BF16 ? (amax_s << 16) : amax_s;
-    uint32_t fl;
-    const int32_t bx = bias_of<FMT>(a32, margin, &fl);
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-        *bias = bx;
-        if (amax_bits) *amax_bits = a32;
-        if (flags) *flags = fl;
+    quant_pass2_body<DT, FMT>(blockIdx.x, gridDim.x, tile, red, amax_s, x, rows, cols, ldx, parts, nparts, used,
+                              have_used, margin, bias, amax_bits, flags, q, ldq, qT, ldqT, tiles_c, ncast,
+                              vec_in, vec_q, vec_qT);
+}
+
+// ------------------------------------------------ quantise several tensors
+// fp8_quantise of up to kQBatch tensors of one element type and format in one
+// pass-1 launch and one pass-2 launch: workgroups [t0[i], t0[i+1]) of pass 1
+// are tensor i's tiles, workgroups [p0[i], p0[i+1]) of pass 2 its finishing
+// workgroups; each tensor keeps its own workspace (used word + tile maxima),
+// so the bits are those of separate calls.
+struct QBatch {
+    int n;
+    int64_t t0[kQBatch + 1], p0[kQBatch + 1];
+    const void* x[kQBatch];
+    int64_t rows[kQBatch], cols[kQBatch], ldx[kQBatch], tiles_c[kQBatch];
+    const int32_t* pred[kQBatch];
+    int32_t* bias[kQBatch];
+    uint32_t* amax[kQBatch];
+    uint32_t* flags[kQBatch];
+    uint8_t* q[kQBatch];
+    int64_t ldq[kQBatch];
+    uint8_t* qT[kQBatch];
+    int64_t ldqT[kQBatch];
+    uint32_t* ws[kQBatch];
+    int vec_in[kQBatch], vec_q[kQBatch], vec_qT[kQBatch];
+};
+
+__device__ __forceinline__ int batch_slot(const int64_t* start, int n, int64_t b) {
+    int i = 0;
+    while (i + 1 < n && b >= start[i + 1]) ++i;
+    return i;
+}
+
+template <int DT, int FMT, bool CAST>
+__global__ __launch_bounds__(kCastThreads) void quant_pass1_batch_kernel(QBatch qb) {
+    __shared__ __attribute__((aligned(16))) uint8_t tile[kCastCols * kCastRows];
+    __shared__ uint32_t red[kCastThreads / 64];
+    const int i = batch_slot(qb.t0, qb.n, blockIdx.x);
+    const int64_t t = (int64_t)blockIdx.x - qb.t0[i];
+    int b = 0;
+    if (CAST) {
+        b = clamp_bias(*qb.pred[i]);
+        if (t == 0 && threadIdx.x == 0) *(int32_t*)qb.ws[i] = b;
     }
-    const int b = clamp_bias(bx);
-    if (have_used && *used == b) return;  // pass 1 already wrote these codes
-    for (int64_t t = blockIdx.x; t < ncast; t += gridDim.x)
-        cast_tile<DT, FMT, false>(x, rows, cols, ldx, b, q, ldq, qT, ldqT, t / tiles_c, t % tiles_c,
-                                  vec_in, vec_q, vec_qT, tile);
+    const uint32_t m = cast_tile<DT, FMT, true>(qb.x[i], qb.rows[i], qb.cols[i], qb.ldx[i], b, CAST ? qb.q[i] : nullptr,
+                                                qb.ldq[i], CAST ? qb.qT[i] : nullptr, qb.ldqT[i], t / qb.tiles_c[i],
+                                                t % qb.tiles_c[i], qb.vec_in[i], qb.vec_q[i], qb.vec_qT[i], tile);
+    const uint32_t bm = block_max(m, red);
+    if (threadIdx.x == 0) qb.ws[i][1 + t] = bm;
+}
+
+template <int DT, int FMT>
+__global__ __launch_bounds__(kCastThreads) void quant_pass2_batch_kernel(QBatch qb, int32_t margin, int have_used) {
+    __shared__ __attribute__((aligned(16))) uint8_t tile[kCastCols * kCastRows];
+    __shared__ uint32_t red[kCastThreads / 64];
+    __shared__ uint32_t amax_s;
+    const int i = batch_slot(qb.p0, qb.n, blockIdx.x);
+    const int64_t ntiles = qb.t0[i + 1] - qb.t0[i];
+    quant_pass2_body<DT, FMT>((int)(blockIdx.x - qb.p0[i]), (int)(qb.p0[i + 1] - qb.p0[i]), tile, red, amax_s,
+                              qb.x[i], qb.rows[i], qb.cols[i], qb.ldx[i], qb.ws[i] + 1, (int)ntiles,
+                              (const int32_t*)qb.ws[i], have_used, margin, qb.bias[i], qb.amax[i], qb.flags[i],
+                              qb.q[i], qb.ldq[i], qb.qT[i], qb.ldqT[i], qb.tiles_c[i], ntiles, qb.vec_in[i],
+                              qb.vec_q[i], qb.vec_qT[i]);
 }
 
 template <int DT, int FMT>
@@ -372,6 +447,46 @@ void launch_quantise_t(const void* x, int64_t rows, int64_t cols, int64_t ldx, i
     hipLaunchKernelGGL((quant_pass2_kernel<DT, FMT>), dim3(nb2), dim3(kCastThreads), 0, s, x, rows, cols, ldx,
                        parts, (int)ntiles, used, bias_pred ? 1 : 0, margin, bias, amax_bits, flags, q, ldq,
                        qT, ldqT, tiles_c, ntiles, vec_in, vec_q, vec_qT);
+}
+
+template <int DT, int FMT>
+void launch_quantise_batch_t(int n, const QuantDesc* d, int32_t margin, hipStream_t s) {
+    QBatch qb{};
+    qb.n = n;
+    const int esz = DT == FP8_DT_BF16 ? 2 : 4;
+    bool pred = false;
+    for (int i = 0; i < n; ++i) {
+        const int64_t tiles_c = (d[i].cols + kCastCols - 1) / kCastCols;
+        const int64_t ntiles = ((d[i].rows + kCastRows - 1) / kCastRows) * tiles_c;
+        qb.t0[i + 1] = qb.t0[i] + ntiles;
+        qb.p0[i + 1] = qb.p0[i] + (ntiles < kQuantPass2MaxBlocks ? ntiles : kQuantPass2MaxBlocks);
+        qb.x[i] = d[i].x;
+        qb.rows[i] = d[i].rows;
+        qb.cols[i] = d[i].cols;
+        qb.ldx[i] = d[i].ldx;
+        qb.tiles_c[i] = tiles_c;
+        qb.pred[i] = d[i].pred;
+        qb.bias[i] = d[i].bias;
+        qb.amax[i] = d[i].amax;
+        qb.flags[i] = d[i].flags;
+        qb.q[i] = d[i].q;
+        qb.ldq[i] = d[i].ldq;
+        qb.qT[i] = d[i].qT;
+        qb.ldqT[i] = d[i].ldqT;
+        qb.ws[i] = d[i].ws;
+        qb.vec_in[i] = ((uintptr_t)d[i].x % 16 == 0) && ((d[i].ldx * esz) % 16 == 0);
+        qb.vec_q[i] = d[i].q && ((uintptr_t)d[i].q % 8 == 0) && (d[i].ldq % 8 == 0);
+        qb.vec_qT[i] = d[i].qT && ((uintptr_t)d[i].qT % 16 == 0) && (d[i].ldqT % 16 == 0);
+        pred = d[i].pred != nullptr;
+    }
+    if (pred)
+        hipLaunchKernelGGL((quant_pass1_batch_kernel<DT, FMT, true>), dim3((unsigned)qb.t0[n]), dim3(kCastThreads), 0,
+                           s, qb);
+    else
+        hipLaunchKernelGGL((quant_pass1_batch_kernel<DT, FMT, false>), dim3((unsigned)qb.t0[n]), dim3(kCastThreads),
+                           0, s, qb);
+    hipLaunchKernelGGL((quant_pass2_batch_kernel<DT, FMT>), dim3((unsigned)qb.p0[n]), dim3(kCastThreads), 0, s, qb,
+                       margin, pred ? 1 : 0);
 }
 
 template <int DT, int FMT>
@@ -641,6 +756,13 @@ int32_t launch_quantise(const void* x, int dt, int64_t rows, int64_t cols, int64
     with_dt_fmt(dt, fmt, [&](auto D, auto F) {
         launch_quantise_t<decltype(D)::value, decltype(F)::value>(x, rows, cols, ldx, margin, bias_pred, bias, amax_bits,
                                                                   flags, q, ldq, qT, ldqT, ws, s);
+    });
+    return hip_status();
+}
+
+int32_t launch_quantise_batch(int n, const QuantDesc* d, int dt, int fmt, int32_t margin, hipStream_t s) {
+    with_dt_fmt(dt, fmt, [&](auto D, auto F) {
+        launch_quantise_batch_t<decltype(D)::value, decltype(F)::value>(n, d, margin, s);
     });
     return hip_status();
 }

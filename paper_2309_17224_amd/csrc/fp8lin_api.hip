@@ -149,6 +149,44 @@ int32_t fp8_quantise(const void* x, int32_t dt, int64_t rows, int64_t cols, int6
                            q, ldq, qT, ldqT, (uint32_t*)ws, as_stream(stream));
 }
 
+int32_t fp8_quantise_batch(int32_t n, const fp8_quantise_args* t, int32_t dt, int32_t fmt, int32_t margin,
+                           void* stream) {
+    if (n == 0) return FP8_OK;
+    if (n < 0 || n > FP8_QUANTISE_BATCH_MAX || !t) return FP8_EINVAL;
+    if (!dt_ok(dt) || !fmt_ok(fmt) || margin > FP8_MAX_MARGIN || margin < -FP8_MAX_MARGIN) return FP8_EINVAL;
+    QuantDesc d[kQBatch];
+    int m = 0, npred = 0;
+    int64_t tiles = 0;
+    for (int i = 0; i < n; ++i) {
+        const fp8_quantise_args& a = t[i];
+        if (a.rows < 0 || a.cols < 0 || a.rows > kMaxDim || a.cols > kMaxDim) return FP8_EINVAL;
+        if (!a.bias || !aligned(a.bias, 4)) return FP8_EINVAL;
+        if ((a.amax_bits && !aligned(a.amax_bits, 4)) || (a.flags && !aligned(a.flags, 4))) return FP8_EINVAL;
+        if (a.bias_pred && !aligned(a.bias_pred, 4)) return FP8_EINVAL;
+        if (a.rows == 0 || a.cols == 0) continue;  // handled below, like fp8_quantise
+        if (!a.x || (!a.q && !a.qT) || !a.ws) return FP8_EINVAL;
+        if (!aligned(a.x, esize(dt)) || !aligned(a.ws, 4)) return FP8_EINVAL;
+        if (a.ldx < a.cols || (a.q && a.ldq < a.cols) || (a.qT && a.ldqT < a.rows)) return FP8_EINVAL;
+        if (a.ws_bytes < fp8_quantise_ws_bytes(a.rows, a.cols)) return FP8_EINVAL;
+        if (quantise_ws_words(a.rows, a.cols) - 1 > INT32_MAX) return FP8_ENOTSUP;
+        tiles += quantise_ws_words(a.rows, a.cols) - 1;
+        npred += a.bias_pred ? 1 : 0;
+        d[m++] = QuantDesc{a.x, a.rows, a.cols, a.ldx, a.bias_pred, a.bias, a.amax_bits, a.flags,
+                           a.q, a.ldq, a.qT, a.ldqT, (uint32_t*)a.ws};
+    }
+    if (npred != 0 && npred != m) return FP8_EINVAL;
+    if (tiles > INT32_MAX) return FP8_ENOTSUP;
+    for (int i = 0; i < n; ++i) {
+        const fp8_quantise_args& a = t[i];
+        if (a.rows == 0 || a.cols == 0) {
+            const int32_t st = launch_scale_bias(a.x, dt, 0, fmt, margin, a.bias, a.amax_bits, a.flags, nullptr,
+                                                 as_stream(stream));
+            if (st != FP8_OK) return st;
+        }
+    }
+    return m > 0 ? launch_quantise_batch(m, d, dt, fmt, margin, as_stream(stream)) : FP8_OK;
+}
+
 int32_t fp8_bias_from_amax(const uint32_t* amax_bits, int32_t fmt, int32_t margin, int32_t* bias,
                            uint32_t* flags, void* stream) {
     if (!fmt_ok(fmt) || margin < -FP8_MAX_MARGIN || margin > FP8_MAX_MARGIN) return FP8_EINVAL;

@@ -28,6 +28,23 @@ int32_t launch_cast(const void* x, int dt, int64_t rows, int64_t cols, int64_t l
 // amax + bias + cast of a rows x cols tensor (two kernels); ws holds
 // quantise_ws_words(rows, cols) uint32 words.
 int64_t quantise_ws_words(int64_t rows, int64_t cols);
+
+// fp8_quantise of several tensors of one type and format (checked arguments).
+constexpr int kQBatch = FP8_QUANTISE_BATCH_MAX;
+struct QuantDesc {
+    const void* x;
+    int64_t rows, cols, ldx;
+    const int32_t* pred;
+    int32_t* bias;
+    uint32_t* amax;
+    uint32_t* flags;
+    uint8_t* q;
+    int64_t ldq;
+    uint8_t* qT;
+    int64_t ldqT;
+    uint32_t* ws;
+};
+int32_t launch_quantise_batch(int n, const QuantDesc* d, int dt, int fmt, int32_t margin, hipStream_t s);
 int32_t launch_quantise(const void* x, int dt, int64_t rows, int64_t cols, int64_t ldx, int fmt,
                         int32_t margin, const int32_t* bias_pred, int32_t* bias, uint32_t* amax_bits,
                         uint32_t* flags, uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT,

@@ -28,6 +28,7 @@ EXPORTS = (
     "fp8_status_string", "fp8_abi_version", "fp8_scale_bias_ws_bytes", "fp8_scale_bias",
     "fp8_bias_from_amax", "fp8_cast_e4", "fp8_cast_e5", "fp8_cast", "fp8_quantise_ws_bytes",
     "fp8_quantise",
+    "fp8_quantise_batch",
     "fp8_linear_fwd", "fp8_linear_bwd_dx", "fp8_linear_bias_ws_bytes", "fp8_linear_fwd_bias",
     "fp8_linear_bwd_dx_bias", "fp8_linear_quantise_ws_bytes",
     "fp8_linear_fwd_quantise", "fp8_linear_bwd_dx_quantise",
@@ -77,6 +78,8 @@ def lib() -> ctypes.CDLL:
         L.fp8_quantise.restype = i32
         L.fp8_quantise.argtypes = [vp, i32, i64, i64, i64, i32, i32, vp, vp, vp, vp, vp, i64, vp,
                                    i64, vp, sz, vp]
+        L.fp8_quantise_batch.argtypes = [i32, vp, i32, i32, i32, vp]
+        L.fp8_quantise_batch.restype = i32
         for name in ("fp8_linear_fwd", "fp8_linear_bwd_dx"):
             f = getattr(L, name)
             f.restype = i32
@@ -273,6 +276,38 @@ def fp8_quantise(x: torch.Tensor, fmt: int, margin: int = 0, bias_pred=None, bia
                             ws.numel() * ws.element_size(), _stream(stream))
     _check("fp8_quantise", st)
     return q, qT, bias, amax_bits, flags
+
+
+class QuantiseArgs(ctypes.Structure):
+    """fp8_quantise_args of the C header (device pointers, sizes)."""
+    _fields_ = [("x", ctypes.c_void_p), ("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
+                ("ldx", ctypes.c_int64), ("bias_pred", ctypes.c_void_p), ("bias", ctypes.c_void_p),
+                ("amax_bits", ctypes.c_void_p), ("flags", ctypes.c_void_p), ("q", ctypes.c_void_p),
+                ("ldq", ctypes.c_int64), ("qT", ctypes.c_void_p), ("ldqT", ctypes.c_int64),
+                ("ws", ctypes.c_void_p), ("ws_bytes", ctypes.c_size_t)]
+
+
+QUANTISE_BATCH_MAX = 4
+
+
+def fp8_quantise_batch(items, fmt: int, margin: int = 0, stream=None):
+    """fp8_quantise of several 2-D tensors of one dtype in two launches (same
+    bits as separate calls).  items: dicts with x, bias, ws and optionally
+    bias_pred, amax_bits, flags, q, qT (outputs are not allocated here)."""
+    arr = (QuantiseArgs * max(len(items), 1))()
+    dt = _dt(items[0]["x"]) if items else DT_BF16
+    for a, it in zip(arr, items):
+        x = it["x"]
+        q, qT, ws = it.get("q"), it.get("qT"), it["ws"]
+        a.x, a.rows, a.cols, a.ldx = _p(x), x.shape[0], x.shape[1], _ld(x)
+        a.bias_pred, a.bias = _p(it.get("bias_pred")), _p(it["bias"])
+        a.amax_bits, a.flags = _p(it.get("amax_bits")), _p(it.get("flags"))
+        a.q, a.ldq = _p(q), _ld(q) if q is not None else 0
+        a.qT, a.ldqT = _p(qT), _ld(qT) if qT is not None else 0
+        a.ws, a.ws_bytes = _p(ws), ws.numel() * ws.element_size()
+    st = lib().fp8_quantise_batch(len(items), ctypes.cast(arr, ctypes.c_void_p), dt, fmt, margin,
+                                  _stream(stream))
+    _check("fp8_quantise_batch", st)
 
 
 def _out(shape, out_dt, dev, out):

@@ -231,3 +231,33 @@ def test_decoder_glue_rejects(L):
     assert L.llama_residual_add(A, A, A, 12, NULL) == F.EINVAL
     assert L.llama_residual_add(A, ODD, A, 16, NULL) == F.EINVAL
     assert L.llama_residual_add(NULL, NULL, NULL, 0, NULL) == F.OK
+
+
+def test_quantise_batch_rejects(L):
+    """fp8_quantise_batch checks every tensor as fp8_quantise does, plus the
+    batch size and that predictions are given for all tensors or none."""
+    def args(**kw):
+        a = F.QuantiseArgs(x=FAKE, rows=4, cols=8, ldx=8, bias_pred=None, bias=FAKE, amax_bits=None,
+                           flags=None, q=FAKE, ldq=8, qT=None, ldqT=0, ws=FAKE, ws_bytes=4 * 64)
+        for k, v in kw.items():
+            setattr(a, k, v)
+        return a
+
+    def call(items, n=None, dt=0, fmt=0, margin=0):
+        arr = (F.QuantiseArgs * max(len(items), 1))(*items)
+        return L.fp8_quantise_batch(len(items) if n is None else n, ctypes.cast(arr, ctypes.c_void_p), dt, fmt,
+                                    margin, NULL)
+
+    assert L.fp8_quantise_batch(0, NULL, 0, 0, 0, NULL) == F.OK            # nothing to do
+    assert L.fp8_quantise_batch(1, NULL, 0, 0, 0, NULL) == F.EINVAL        # no array
+    assert call([args()] * 5) == F.EINVAL                                  # more than the maximum
+    assert call([args()], n=-1) == F.EINVAL
+    assert call([args(), args(ldx=7)]) == F.EINVAL                         # second tensor's stride
+    assert call([args(), args(ws_bytes=4)]) == F.EINVAL                    # second tensor's workspace
+    assert call([args(), args(q=None)]) == F.EINVAL                        # no output
+    assert call([args(bias=None)]) == F.EINVAL
+    assert call([args(bias_pred=FAKE), args()]) == F.EINVAL                # mixed predictions
+    assert call([args()], dt=3) == F.EINVAL
+    assert call([args()], fmt=4) == F.EINVAL
+    assert call([args()], margin=1 << 20) == F.EINVAL
+    assert F.QUANTISE_BATCH_MAX == 4 and "FP8_QUANTISE_BATCH_MAX 4" in open(HEADER).read()
