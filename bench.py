@@ -69,6 +69,9 @@ def parse():
                    help="decoder-layer workloads: one activation bias per tensor and call (quantise fused "
                         "into the producing kernels), or one per sequence (segmented quantise, per-row-bias "
                         "matmuls)")
+    p.add_argument("--no-quant-batch", action="store_true",
+                   help="one fp8_quantise call per tensor instead of fp8_quantise_batch over the "
+                        "tensors of each quantise phase (identical bits)")
     p.add_argument("--amax-mb", type=int, default=0,
                    help="only time fp8_scale_bias on a bf16 tensor of this many MB, --steps calls "
                         "(read-bandwidth reference for the amax kernel), then exit")
@@ -414,7 +417,7 @@ def main():
     torch.cuda.synchronize()
     step = L.WorkloadStep(w, tens, dev, margin=args.margin, quant=args.quant,
                           cscale_bias=args.cscale_bias, fused_bias=args.bias == "fused",
-                          concurrent=args.streams == 2)
+                          concurrent=args.streams == 2, batch_quant=not args.no_quant_batch)
     if not w.train:
         step.prepare_inference()
     flush = None
@@ -445,7 +448,7 @@ def main():
                    "linears": [dict(name=l.name, M=l.M, K=l.K, N=l.N) for l in w.linears],
                    "mode": "train fwd+bwd" if w.train else "PTQ inference fwd",
                    "accumulate": "fp32", "outputs": "Y,dX bf16; dW fp32",
-                   "margin": args.margin, "mall_flush_mb": args.flush_mb, "quant": args.quant,
+                   "margin": args.margin, "mall_flush_mb": args.flush_mb, "quant": args.quant, "quant_batch": not args.no_quant_batch,
                    "output_bias": args.bias,
                    "launch": (f"one HIP graph replay per step, {args.streams} stream(s)" if args.launch == "graph"
                               else "one host call per library call")},

@@ -182,6 +182,11 @@ class WorkloadStep:
     fused_bias: the forward and grad-input matmuls take the bias of their
       outputs in the same launch (fp8_linear_fwd_bias / fp8_linear_bwd_dx_bias);
       False: epilogue amax, then fp8_bias_from_amax (identical bits).
+    batch_quant: with "predicted" or "twopass" and one stream, the tensors of
+      one quantise phase (weights and activations before the forward
+      matmuls; gradients before the backward ones) go through
+      fp8_quantise_batch, up to four per call: two launches instead of two
+      per tensor, same bits.
     concurrent: capture() records independent calls on two streams (the
       quantise calls of the weights and activations, those of the gradients,
       and each linear's grad-input and grad-weight matmuls), so that the last
@@ -195,7 +200,8 @@ class WorkloadStep:
     QUANT_MODES = ("predicted", "twopass", "separate", "cscale")
 
     def __init__(self, workload, tensors: dict, device, margin: int = 0, quant: str = "predicted",
-                 cscale_bias: int = 0, fused_bias: bool = True, concurrent: bool = False):
+                 cscale_bias: int = 0, fused_bias: bool = True, concurrent: bool = False,
+                 batch_quant: bool = True):
         if quant not in self.QUANT_MODES:
             raise ValueError(f"quant must be one of {self.QUANT_MODES}")
         self.fused_bias = bool(fused_bias)
@@ -235,6 +241,7 @@ class WorkloadStep:
             qt.qws = torch.empty(max(F.fp8_quantise_ws_bytes(*x.shape), 4), dtype=torch.uint8, device=device)
             qt.sws = F.workspace(x.numel(), device)
         self.concurrent = bool(concurrent) and self.dev.type == "cuda"
+        self.batch_quant = bool(batch_quant) and not self.concurrent and quant in ("predicted", "twopass")
         self.side = torch.cuda.Stream(self.dev) if self.concurrent else None  # default priority
         self.sched = []
         self.calls = self._build()
@@ -267,6 +274,23 @@ class WorkloadStep:
                           want_qT=qt.qT is not None)),
         ]
 
+    def _quant_batch(self, names, fmt, margin):
+        """The quantise calls of `names`, up to QUANTISE_BATCH_MAX tensors per
+        fp8_quantise_batch call."""
+        calls = []
+        for g in range(0, len(names), F.QUANTISE_BATCH_MAX):
+            grp = names[g:g + F.QUANTISE_BATCH_MAX]
+            items, work = [], 0
+            for name in grp:
+                x, qt = self.t[name], self.q[name]
+                n = x.numel()
+                work += 2 * n + n + (n if qt.qT is not None and qt.q is not None else 0)
+                items.append(dict(x=x, bias=qt.bias, bias_pred=qt.bias if self.quant == "predicted" else None,
+                                  amax_bits=qt.amax, flags=qt.flags, q=qt.q, qT=qt.qT, ws=qt.qws))
+            calls.append((f"quantise {'+'.join(grp)}", "quantise", work,
+                          lambda items=items: F.fp8_quantise_batch(items, fmt, margin)))
+        return calls
+
     def _build(self):
         """The step's calls in issue order; self.sched[i] = (phase, branch) of
         call i: consecutive calls of one phase are independent across branches
@@ -280,17 +304,14 @@ class WorkloadStep:
         lin = self.w.linears
         done = set()
         weights = [l.w for l in lin]
-        nq = 0
-        if self.w.train:
-            for name in dict.fromkeys(weights):
+        names = list(dict.fromkeys(weights)) if self.w.train else []
+        names += [x for x in dict.fromkeys(l.x for l in lin) if x not in names]
+        done.update(names)
+        if self.batch_quant:
+            add(self._quant_batch(names, F.E4M3, 0), "quantise inputs")
+        else:
+            for nq, name in enumerate(names):
                 add(self._quant(name, F.E4M3, 0), "quantise inputs", nq % 2)
-                nq += 1
-                done.add(name)
-        for l in lin:
-            if l.x not in done:
-                add(self._quant(l.x, F.E4M3, 0), "quantise inputs", nq % 2)
-                nq += 1
-                done.add(l.x)
         for l in lin:
             xq, wq, o = self.q[l.x], self.q[l.w], self.out[l.name]
             flop = 2 * l.M * l.N * l.K
@@ -317,12 +338,13 @@ class WorkloadStep:
                                                        bias=o["y_scal"][0:1],
                                                        flags=o["y_scal"][2:3]))])
         if self.w.train:
-            nq = 0
-            for l in lin:
-                if l.dy not in done:
-                    add(self._quant(l.dy, F.E5M2, self.margin), "quantise gradients", nq % 2)
-                    nq += 1
-                    done.add(l.dy)
+            grads = [g for g in dict.fromkeys(l.dy for l in lin) if g not in done]
+            done.update(grads)
+            if self.batch_quant:
+                add(self._quant_batch(grads, F.E5M2, self.margin), "quantise gradients")
+            else:
+                for nq, name in enumerate(grads):
+                    add(self._quant(name, F.E5M2, self.margin), "quantise gradients", nq % 2)
             for l in lin:
                 xq, wq, gq, o = self.q[l.x], self.q[l.w], self.q[l.dy], self.out[l.name]
                 flop = 2 * l.M * l.N * l.K

@@ -168,3 +168,83 @@ def test_quantise_workspace_reused(orc, gpu):
         torch.cuda.synchronize()
         assert (i32(b), u32(a), u32(fl)) == (ob, oa, ofl)
         assert np.array_equal(q.cpu().numpy(), oq) and np.array_equal(qT.cpu().numpy(), oqT)
+
+
+@pytest.mark.parametrize("fmt", [F.E4M3, F.E5M2], ids=["e4", "e5"])
+@pytest.mark.parametrize("preds", [None, (0, 0, 0, 0), (0, 2, -1, "alias")], ids=["none", "right", "mixed"])
+def test_quantise_batch_equals_separate_calls(orc, gpu, fmt, preds):
+    """fp8_quantise_batch over ragged, strided, codes-only and transposed-only
+    tensors (and an empty one) gives, for each tensor, the oracle's bits and
+    the bits of a separate fp8_quantise call, whatever its prediction."""
+    from paper_2309_17224_amd import workloads as wl
+    shapes = [(300, 520, 1.0, True, True), (129, 1000, 40.0, True, False), (64, 64, 3e-3, False, True),
+              (200, 300, 0.5, True, True)]
+    items, expect = [], []
+    for k, (rows, cols, std, want_q, want_qT) in enumerate(shapes):
+        x = wl.small(rows, cols, std, 10 + k)
+        if k == 3:  # strided: the first 300 columns of a wider tensor
+            wide = wl.small(rows, 320, std, 20).to(gpu)
+            wide[:, :cols] = x.to(gpu)
+            xd = wide[:, :cols]
+        else:
+            xd = x.to(gpu)
+        ob, oa, ofl, oq, oqT = oracle_expect(orc, x, fmt)
+        bias = torch.zeros(1, dtype=torch.int32, device=gpu)
+        pred = None
+        if preds is not None:
+            p = preds[k]
+            if p == "alias":
+                bias.fill_(ob - 3)
+                pred = bias
+            else:
+                pred = torch.tensor([ob + p], dtype=torch.int32, device=gpu)
+        it = dict(x=xd, bias=bias, bias_pred=pred, amax_bits=torch.zeros(1, dtype=torch.int32, device=gpu),
+                  flags=torch.zeros(1, dtype=torch.int32, device=gpu),
+                  q=torch.empty((rows, cols), dtype=torch.uint8, device=gpu) if want_q else None,
+                  qT=torch.empty((cols, rows), dtype=torch.uint8, device=gpu) if want_qT else None,
+                  ws=F.quantise_workspace(rows, cols, gpu))
+        items.append(it)
+        expect.append((ob, oa, ofl, oq if want_q else None, oqT if want_qT else None))
+    empty = dict(x=torch.empty((0, 8), dtype=torch.bfloat16, device=gpu),
+                 bias=torch.full((1,), 9, dtype=torch.int32, device=gpu),
+                 flags=torch.zeros(1, dtype=torch.int32, device=gpu),
+                 q=torch.empty((0, 8), dtype=torch.uint8, device=gpu), ws=torch.empty(4, dtype=torch.uint8, device=gpu))
+    F.fp8_quantise_batch(items[:2] + [empty], fmt)
+    F.fp8_quantise_batch(items[2:], fmt)
+    torch.cuda.synchronize()
+    assert i32(empty["bias"]) == 0 and u32(empty["flags"]) == F.FLAG_ZERO
+    for it, (ob, oa, ofl, oq, oqT) in zip(items, expect):
+        assert (i32(it["bias"]), u32(it["amax_bits"]), u32(it["flags"])) == (ob, oa, ofl)
+        if oq is not None:
+            assert np.array_equal(it["q"].cpu().numpy(), oq)
+        if oqT is not None:
+            assert np.array_equal(it["qT"].cpu().numpy(), oqT)
+        # the same call alone
+        q, qT, b, a, fl = F.fp8_quantise(it["x"], fmt, 0, want_q=oq is not None, want_qT=oqT is not None)
+        torch.cuda.synchronize()
+        assert (i32(b), u32(a), u32(fl)) == (ob, oa, ofl)
+        if oq is not None:
+            assert torch.equal(q, it["q"])
+        if oqT is not None:
+            assert torch.equal(qT, it["qT"])
+
+
+def test_quantise_batch_four_large_tensors(orc, gpu):
+    """Four tensors whose tiles exceed the pass-2 workgroup cap each (a
+    misprediction makes every tensor's finishing workgroups recast it)."""
+    from paper_2309_17224_amd import workloads as wl
+    items, ref = [], []
+    for k, (rows, cols) in enumerate([(2048, 1024), (1024, 2304), (640, 3000), (4096, 512)]):
+        x = wl.small(rows, cols, 1.0 + k, 30 + k)
+        ob, oa, ofl, oq, oqT = oracle_expect(orc, x, F.E4M3)
+        items.append(dict(x=x.to(gpu), bias=torch.zeros(1, dtype=torch.int32, device=gpu),
+                          bias_pred=torch.tensor([ob + (k % 2)], dtype=torch.int32, device=gpu),
+                          q=torch.empty((rows, cols), dtype=torch.uint8, device=gpu),
+                          qT=torch.empty((cols, rows), dtype=torch.uint8, device=gpu),
+                          ws=F.quantise_workspace(rows, cols, gpu)))
+        ref.append((ob, oq, oqT))
+    F.fp8_quantise_batch(items, F.E4M3)
+    torch.cuda.synchronize()
+    for it, (ob, oq, oqT) in zip(items, ref):
+        assert i32(it["bias"]) == ob
+        assert np.array_equal(it["q"].cpu().numpy(), oq) and np.array_equal(it["qT"].cpu().numpy(), oqT)
