@@ -182,11 +182,11 @@ class WorkloadStep:
     fused_bias: the forward and grad-input matmuls take the bias of their
       outputs in the same launch (fp8_linear_fwd_bias / fp8_linear_bwd_dx_bias);
       False: epilogue amax, then fp8_bias_from_amax (identical bits).
-    batch_quant: with "predicted" or "twopass" and one stream, the tensors of
-      one quantise phase (weights and activations before the forward
-      matmuls; gradients before the backward ones) go through
-      fp8_quantise_batch, up to four per call: two launches instead of two
-      per tensor, same bits.
+    batch_quant: with "predicted" or "twopass" and one stream, the weight and
+      the input of each linear, which are ready together before its forward
+      matmul, go through one fp8_quantise_batch call: two launches instead of
+      four, same bits.  Tensors of different linears are never batched (in a
+      network one linear's input is produced by the linear before it).
     concurrent: capture() records independent calls on two streams (the
       quantise calls of the weights and activations, those of the gradients,
       and each linear's grad-input and grad-weight matmuls), so that the last
@@ -306,10 +306,14 @@ class WorkloadStep:
         weights = [l.w for l in lin]
         names = list(dict.fromkeys(weights)) if self.w.train else []
         names += [x for x in dict.fromkeys(l.x for l in lin) if x not in names]
-        done.update(names)
         if self.batch_quant:
-            add(self._quant_batch(names, F.E4M3, 0), "quantise inputs")
+            for l in lin:  # one call per linear: its weight and input
+                grp = [n for n in ((l.w,) if self.w.train else ()) + (l.x,) if n not in done]
+                done.update(grp)
+                if grp:
+                    add(self._quant_batch(grp, F.E4M3, 0), "quantise inputs")
         else:
+            done.update(names)
             for nq, name in enumerate(names):
                 add(self._quant(name, F.E4M3, 0), "quantise inputs", nq % 2)
         for l in lin:
@@ -340,11 +344,9 @@ class WorkloadStep:
         if self.w.train:
             grads = [g for g in dict.fromkeys(l.dy for l in lin) if g not in done]
             done.update(grads)
-            if self.batch_quant:
-                add(self._quant_batch(grads, F.E5M2, self.margin), "quantise gradients")
-            else:
-                for nq, name in enumerate(grads):
-                    add(self._quant(name, F.E5M2, self.margin), "quantise gradients", nq % 2)
+            for nq, name in enumerate(grads):  # each gradient on its own
+                add(self._quant_batch([name], F.E5M2, self.margin) if self.batch_quant
+                    else self._quant(name, F.E5M2, self.margin), "quantise gradients", nq % 2)
             for l in lin:
                 xq, wq, gq, o = self.q[l.x], self.q[l.w], self.q[l.dy], self.out[l.name]
                 flop = 2 * l.M * l.N * l.K
