@@ -95,8 +95,9 @@ __global__ __launch_bounds__(kThreads) void add_kernel(const uint16_t* __restric
 // ------------------------------------------------------------- RMSNorm
 // One workgroup per row.  h = x (+ res), rounded; y = h / sqrt(mean(h^2) + eps)
 // * g.  The sum of squares is taken in fp32 in a fixed order (each lane its
-// elements in order, then a fixed reduction tree); the row is read twice, the
-// second time from L2.
+// elements in order, then a fixed reduction tree).  Rows of up to
+// 8 x 8 x kThreads columns are held in registers (all loads issued at once,
+// one read of the row); longer rows are read twice, the second time from L2.
 template <bool RES>
 __device__ __forceinline__ uint4 row_h8(const uint16_t* x, const uint16_t* res) {
     const uint4 v = ld16(x);
@@ -125,8 +126,28 @@ __global__ __launch_bounds__(kThreads) void rmsnorm_kernel(
     const int64_t r = blockIdx.x;
     const uint16_t* xr = x + r * ldx;
     const uint16_t* rr = RES ? res + r * ldr : nullptr;
+    constexpr int kChunks = 8;
+    const bool in_regs = cols <= (int64_t)8 * kThreads * kChunks;
+    uint4 hr[kChunks], gr[kChunks];
     float ss = 0.0f;
-    for (int64_t c = 8 * threadIdx.x; c < cols; c += 8 * kThreads) ss = sumsq8(row_h8<RES>(xr + c, rr + c), ss);
+    if (in_regs) {
+        // unconditional loads (the last chunk of the row is in bounds: cols is
+        // a nonzero multiple of 8), chunks past the end zeroed afterwards
+#pragma unroll
+        for (int k = 0; k < kChunks; ++k) {
+            const int64_t c = min((int64_t)8 * (threadIdx.x + kThreads * k), cols - 8);
+            hr[k] = row_h8<RES>(xr + c, rr + c);
+        }
+#pragma unroll
+        for (int k = 0; k < kChunks; ++k) gr[k] = ld16(g + min((int64_t)8 * (threadIdx.x + kThreads * k), cols - 8));
+#pragma unroll
+        for (int k = 0; k < kChunks; ++k) {
+            if (8 * (threadIdx.x + kThreads * k) >= cols) hr[k] = make_uint4(0u, 0u, 0u, 0u);
+            ss = sumsq8(hr[k], ss);
+        }
+    } else {
+        for (int64_t c = 8 * threadIdx.x; c < cols; c += 8 * kThreads) ss = sumsq8(row_h8<RES>(xr + c, rr + c), ss);
+    }
     ss = wave_sum(ss);
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
     __syncthreads();
@@ -136,7 +157,24 @@ __global__ __launch_bounds__(kThreads) void rmsnorm_kernel(
     const bool cast = QUANT && pred;
     const int b = QUANT ? fused_bias(pred, used) : 0;
     uint32_t mag = 0;
-    for (int64_t c = 8 * threadIdx.x; c < cols; c += 8 * kThreads) {
+#pragma unroll
+    for (int k = 0; k < kChunks; ++k) {
+        const int64_t c = (int64_t)8 * (threadIdx.x + kThreads * k);
+        if (!in_regs || c >= cols) break;
+        const uint4 hv = hr[k], gv = gr[k];
+        if (h) st16(h + r * ldh + c, hv);
+        uint4 yv;
+        yv.x = pack_bf16x2(lo_f(hv.x) * rstd * lo_f(gv.x), hi_f(hv.x) * rstd * hi_f(gv.x));
+        yv.y = pack_bf16x2(lo_f(hv.y) * rstd * lo_f(gv.y), hi_f(hv.y) * rstd * hi_f(gv.y));
+        yv.z = pack_bf16x2(lo_f(hv.z) * rstd * lo_f(gv.z), hi_f(hv.z) * rstd * hi_f(gv.z));
+        yv.w = pack_bf16x2(lo_f(hv.w) * rstd * lo_f(gv.w), hi_f(hv.w) * rstd * hi_f(gv.w));
+        st16(y + r * ldy + c, yv);
+        if (QUANT) {
+            mag = max(mag, mag8(yv));
+            if (cast) *(uint2*)(q + r * ldq + c) = codes8<FMT>(yv, b);
+        }
+    }
+    for (int64_t c = 8 * threadIdx.x; !in_regs && c < cols; c += 8 * kThreads) {
         const uint4 hv = row_h8<RES>(xr + c, rr + c);
         if (h) st16(h + r * ldh + c, hv);
         const uint4 gv = ld16(g + c);
