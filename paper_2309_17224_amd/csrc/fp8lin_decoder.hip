@@ -115,7 +115,10 @@ __device__ __forceinline__ float sumsq8(uint4 v, float s) {
     return s;
 }
 
-template <bool RES, bool QUANT, int FMT>
+// CH: 16-byte chunks of the row each lane holds in registers (4 for rows of
+// up to 8192 columns, so that more workgroups fit on a compute unit; 8 up to
+// 16384).
+template <bool RES, bool QUANT, int FMT, int CH>
 __global__ __launch_bounds__(kThreads) void rmsnorm_kernel(
     const uint16_t* __restrict__ x, int64_t ldx, const uint16_t* __restrict__ res, int64_t ldr,
     const uint16_t* __restrict__ g, int64_t cols, float eps, uint16_t* __restrict__ h, int64_t ldh,
@@ -126,7 +129,7 @@ __global__ __launch_bounds__(kThreads) void rmsnorm_kernel(
     const int64_t r = blockIdx.x;
     const uint16_t* xr = x + r * ldx;
     const uint16_t* rr = RES ? res + r * ldr : nullptr;
-    constexpr int kChunks = 8;
+    constexpr int kChunks = CH;
     const bool in_regs = cols <= (int64_t)8 * kThreads * kChunks;
     uint4 hr[kChunks], gr[kChunks];
     float ss = 0.0f;
@@ -686,9 +689,14 @@ int32_t launch_rmsnorm(const uint16_t* x, int64_t ldx, const uint16_t* res, int6
     uint8_t* q = quant ? fq->q : nullptr;
     const int64_t ldq = quant ? fq->ldq : 0;
     auto go = [&](auto R, auto Q, auto F) {
-        hipLaunchKernelGGL((rmsnorm_kernel<decltype(R)::value != 0, decltype(Q)::value != 0, decltype(F)::value>),
-                           dim3((unsigned)rows), dim3(kThreads), 0, s, x, ldx, res, ldr, g, cols, eps, h, ldh, y, ldy,
-                           pred, used, parts, q, ldq);
+        constexpr bool kR = decltype(R)::value != 0, kQ = decltype(Q)::value != 0;
+        constexpr int kF = decltype(F)::value;
+        if (cols <= (int64_t)8 * kThreads * 4)
+            hipLaunchKernelGGL((rmsnorm_kernel<kR, kQ, kF, 4>), dim3((unsigned)rows), dim3(kThreads), 0, s, x, ldx, res,
+                               ldr, g, cols, eps, h, ldh, y, ldy, pred, used, parts, q, ldq);
+        else
+            hipLaunchKernelGGL((rmsnorm_kernel<kR, kQ, kF, 8>), dim3((unsigned)rows), dim3(kThreads), 0, s, x, ldx, res,
+                               ldr, g, cols, eps, h, ldh, y, ldy, pred, used, parts, q, ldq);
     };
     with_fmt(quant ? fq->fmt : FP8_E4M3, [&](auto F) {
         if (res) {

@@ -96,7 +96,7 @@ def test_residual_add_bit_exact(gpu, n):
 
 # ---------------------------------------------------------------- RMSNorm
 @pytest.mark.parametrize("rows,cols,res", [(1, 8, False), (37, 512, False), (64, 8192, True), (300, 1048, True),
-                                           (5, 28672, False)])
+                                           (7, 8200, False), (3, 16384, True), (2, 16392, True), (5, 28672, False)])
 def test_rmsnorm(gpu, orc, rows, cols, res):
     x = rand_bits((rows, cols), 10 + rows)
     r = rand_bits((rows, cols), 20 + rows, 3.0) if res else None
