@@ -368,7 +368,7 @@ def bench_layer(args, cfg):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus %d is not supported"
+        print(json.dumps({"error": "bench.py measures one GPU only; --gpus %d is not supported"
                           % args.gpus}))
         sys.exit(2)
     import torch

@@ -11,7 +11,7 @@ Pins, all derived from Table 7 rather than from either codec:
   NaN (0x7F|s against 0x80) and values rounding to -0 (0x80 against 0x00).
 * With equal biases (E5) the represented values x_hat = dec(q) 2^-b differ
   only for elements below the smallest normal of (b) after scaling.
-The per-workload counts (SURVEY c7) are written by tests/golden/formats_report.py.
+The per-workload counts are written by tests/golden/formats_report.py.
 """
 import numpy as np
 import pytest
