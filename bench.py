@@ -12,9 +12,15 @@ issues one host call per library call instead); a separate eager pass brackets
 every call with HIP events for the per-kernel table.
 
 Prints one JSON line:
-  value      = 6*M*N*K per linear (fwd + bwd matmul FLOPs) / step time, TFLOP/s
+  value      = 6*M*N*K per linear (fwd + bwd matmul FLOPs) / step time, TFLOP/s,
+               on the Llama-2-70B MLP step (gate, up, down; 4096 tokens) by default
   roofline   = the dominant kernel against its roofline, timed with HIP events
   cpu_baseline = the CPU oracle on a bounded sample, extrapolated to one step
+  configs    = the other workloads (GPT-111M, Llama-2-7B up, Llama-2-13B QKV,
+               Llama-2-70B PTQ prefill + decode) timed in the same run
+  mispredicted = the headline step over two input sets whose Eq. 3 biases
+               differ, so that no bias prediction holds (every quantise casts
+               twice)
 """
 from __future__ import annotations
 
@@ -32,10 +38,12 @@ FP8_PEAK_TFLOPS = 5000.0     # MI355X dense FP8 MFMA, published
 BF16_PEAK_TFLOPS = 2500.0    # MI355X dense bf16 MFMA, published
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, published
 METRIC = "FP8 linear fwd+bwd TFLOP/s incl. amax+cast, % of FP8 MFMA peak"
-DEFAULT_WORKLOAD = "llama2-7b-up"
+DEFAULT_WORKLOAD = "llama2-70b-mlp"
+# Workloads timed next to the headline in one default run (fewer steps each).
+SIDE_WORKLOADS = ("gpt111m-linear", "llama2-7b-up", "llama2-13b-qkv", "llama2-70b-ptq")
 
 
-def parse():
+def parse(argv=None):
     p = argparse.ArgumentParser(description=__doc__)
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=50)
@@ -78,7 +86,25 @@ def parse():
     p.add_argument("--copy-mb", type=int, default=0,
                    help="only run a plain device-to-device copy of this many MB, --steps times "
                         "(reference kernel for scaling hardware traffic counters), then exit")
-    return p.parse_args()
+    p.add_argument("--mfma-ceiling", type=int, default=0, metavar="ITERS",
+                   help="only run the register-operand FP8 MFMA loop of libfp8probe.so (ITERS x 8 "
+                        "instructions per wave, 8 waves on each of 256 workgroups), --steps launches: the "
+                        "sustained matrix-core rate with no memory traffic, then exit")
+    p.add_argument("--no-configs", action="store_true",
+                   help="time the chosen workload only (no table of the other workloads)")
+    p.add_argument("--no-mispredicted", action="store_true",
+                   help="skip the step over two input sets whose bias predictions never hold")
+    p.add_argument("--side-steps", type=int, default=20,
+                   help="timed steps of each workload in the configs table")
+    return p.parse_args(argv)
+
+
+def step_kwargs(args) -> dict:
+    """WorkloadStep options of a bench run (the tests build the timed step
+    with these, so that the benchmark times the configuration they check)."""
+    return dict(margin=args.margin, quant=args.quant, cscale_bias=args.cscale_bias,
+                fused_bias=args.bias == "fused", concurrent=args.streams == 2,
+                batch_quant=not args.no_quant_batch)
 
 
 def log(msg):
@@ -274,11 +300,32 @@ def cpu_baseline(w, cpu_tensors, budget_s):
         sampled.append(f"{name}:{nr}/{rows} rows")
     flops = sum(2 * l.M * l.N * l.K * (3 if w.train else 1) for l in w.linears)
     total = t_quant + t_gemm
-    return {"value": round(flops / total / 1e12, 6), "unit": "TFLOP/s", "cores": orc.num_threads(),
+    cores = orc.num_threads()
+    quant_elems = sum(bits[k].size for k in fmt_of)
+    # amax + bias + cast at one thread on the first 2^24 elements of the
+    # largest tensor (the oracle's two passes: amax, then the cast)
+    big = max(fmt_of, key=lambda k: bits[k].size)
+    sample = np.ascontiguousarray(bits[big].reshape(-1)[: 1 << 24])
+    orc.set_num_threads(1)
+    try:
+        t0 = time.perf_counter()
+        b1, _, _ = orc.scale_bias(sample, fmt_of[big])
+        orc.cast(sample, fmt_of[big], b1)
+        t1 = time.perf_counter() - t0
+    finally:
+        orc.set_num_threads(cores)
+    return {"value": round(flops / total / 1e12, 6), "unit": "TFLOP/s", "cores": cores,
             "kind": "oracle",
             "sample": "amax+bias+cast of every tensor in full (%.1fs); matmuls on %s, fp64 "
                       "accumulation, extrapolated by rows to %.1fs" % (t_quant, ", ".join(sampled),
-                                                                     t_gemm)}
+                                                                     t_gemm),
+            "quantise": {"threads": cores, "elements": int(quant_elems), "seconds": round(t_quant, 3),
+                         "GB_per_s": round(3 * quant_elems / t_quant / 1e9, 3),
+                         "note": "amax + bias + cast (codes and transposed codes) of every tensor; "
+                                 "GB/s counts 3 bytes per element"},
+            "quantise_1_thread": {"threads": 1, "elements": int(sample.size), "tensor": big,
+                                  "seconds": round(t1, 3), "GB_per_s": round(3 * sample.size / t1 / 1e9, 3),
+                                  "note": "amax + bias + cast (codes only) of the first 2^24 elements"}}
 
 
 def cpu_baseline_layer(cfg, cpu_tensors, sample_rows=256):
@@ -365,15 +412,168 @@ def bench_layer(args, cfg):
     print(json.dumps(out), flush=True)
 
 
-def main():
-    args = parse()
+def time_alternating(step_a, step_b, steps, warmup):
+    """Wall time per step of replays alternating between two captured steps
+    that share their FP8 buffers (each predicts its biases from the other's
+    last step), and the prediction hits of the last one."""
+    import torch
+    step_a.capture()
+    step_b.capture()
+    for _ in range(max(warmup, 1)):
+        step_a.replay()
+        step_b.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(steps):
+        (step_a if s % 2 == 0 else step_b).replay()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    last = step_a if (steps - 1) % 2 == 0 else step_b
+    return wall / steps, last.prediction_hits()
+
+
+def quantise_table(step, per_call):
+    """Per quantise call: algorithmic bytes (2 read + 1 written per element),
+    average time and rates against HBM peak, with and without the transposed
+    copy of the codes (layout overhead)."""
+    out = []
+    steps = len(per_call)
+    for i, (label, kind, work, _) in enumerate(step.calls):
+        if kind not in ("quantise", "cast", "amax"):
+            continue
+        avg = sum(per_call[s][i] for s in range(steps)) / steps
+        lay = getattr(step, "layout_bytes", {}).get(label, 0)
+        gbs = work / avg / 1e9 if avg > 0 else 0.0
+        out.append({"call": label, "avg_us": round(avg * 1e6, 2), "bytes": int(work), "GB_per_s": round(gbs, 1),
+                    "frac_hbm": round(gbs / HBM_PEAK_GBS, 4), "transpose_bytes": int(lay),
+                    "GB_per_s_incl_transpose": round((work + lay) / avg / 1e9, 1) if avg > 0 else 0.0,
+                    "input_mb": round(2 * work / 3 / 1e6, 1)})
+    return out
+
+
+def input_hashes(cpu):
+    from paper_2309_17224_amd import workloads as wl
+    h = {k: wl.sha256(v) for k, v in cpu.items()}
+    for k, v in h.items():
+        log(f"[bench] input {k} {tuple(cpu[k].shape)} sha256 {v}")
+    return h
+
+
+def bench_workload(args, w, steps, warmup, cpu_baseline_budget=None, mispredicted=False):
+    """Time one linear workload: eager per-call pass (HIP events), then
+    graph replays (or eager steps).  Returns the result fields."""
+    import torch
+    from paper_2309_17224_amd import linear as L
+    dev = torch.device("cuda:0")
+    cpu = make_inputs(w)
+    hashes = input_hashes(cpu)
+    tens = {k: v.to(dev) for k, v in cpu.items()}
+    torch.cuda.synchronize()
+    step = L.WorkloadStep(w, tens, dev, **step_kwargs(args))
+    if not w.train:
+        step.prepare_inference()
+    flush = None
+    if args.flush_mb:
+        flush = torch.zeros(args.flush_mb * (1 << 20) // 4, dtype=torch.float32, device=dev)
+    log(f"[bench] {w.name}: {len(step.calls)} calls per step; warmup {warmup}, steps {steps}")
+    # eager pass: every call bracketed by HIP events on its stream (roofline table)
+    wall, per_call, flush_s = time_steps(step, steps, warmup, flush)
+    eager_step_s = (wall - flush_s) / steps
+    step_s = eager_step_s
+    if args.launch == "graph":
+        gwall, gflush = time_graph(step, steps, warmup, flush)
+        step_s = (gwall - gflush) / steps
+    hits = step.prediction_hits()
+    flops = step.gemm_flops()
+    roof, table = roofline(step, per_call)
+    roof["traffic"] = measured_traffic(w.name, roof["kernel"])
+    for kind, d in sorted(table.items()):
+        log(f"[bench] {kind:11s} " + " ".join(f"{k}={v:.4g}" if isinstance(v, float) else f"{k}={v}"
+                                               for k, v in d.items()))
+    res = {
+        "value": round(flops / step_s / 1e12, 3), "ms_per_step": round(step_s * 1e3, 4),
+        "eager_ms_per_step": round(eager_step_s * 1e3, 4),
+        "frac_of_fp8_peak": round(flops / step_s / 1e12 / FP8_PEAK_TFLOPS, 4),
+        "config": {"workload": w.name, "description": w.description,
+                   "linears": [dict(name=l.name, M=l.M, K=l.K, N=l.N) for l in w.linears],
+                   "mode": "train fwd+bwd" if w.train else "PTQ inference fwd",
+                   "accumulate": "fp32", "outputs": "Y,dX bf16; dW fp32" if w.train else "Y bf16",
+                   "margin": args.margin, "mall_flush_mb": args.flush_mb, "quant": args.quant,
+                   "quant_batch": not args.no_quant_batch, "output_bias": args.bias,
+                   "launch": (f"one HIP graph replay per step, {args.streams} stream(s)" if args.launch == "graph"
+                              else "one host call per library call"),
+                   "inputs_sha256": hashes},
+        "prediction_hits": {"hits": hits[0], "tensors": hits[1],
+                            "note": "last timed step; inputs unchanged between steps"},
+        "roofline": roof,
+        "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv) for kk, vv in d.items()}
+                    for k, d in table.items()},
+        "quantise_calls": quantise_table(step, per_call),
+    }
+    if mispredicted and args.quant == "predicted" and args.launch == "graph":
+        # the same step over 2x the inputs (exact in bf16): every Eq. 3 bias
+        # moves by one, so each replay's predictions (the other set's biases)
+        # fail and every quantise re-casts its tensor
+        tens2 = {k: v * 2 for k, v in tens.items()}
+        step2 = L.WorkloadStep(w, tens2, dev, share=step, **step_kwargs(args))
+        ms, mh = time_alternating(step, step2, steps, warmup)
+        res["mispredicted"] = {"value": round(flops / ms / 1e12, 3), "ms_per_step": round(ms * 1e3, 4),
+                               "prediction_hits": {"hits": mh[0], "tensors": mh[1]},
+                               "inputs": "alternating steps over X, W, dY and over 2 X, 2 W, 2 dY"}
+        del step2, tens2
+    if cpu_baseline_budget is not None:
+        log("[bench] timing the CPU oracle on a bounded sample")
+        res["cpu_baseline"] = cpu_baseline(w, cpu, cpu_baseline_budget)
+    del step, tens
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
+
+
+def mfma_ceiling(args):
+    """Sustained FP8 matrix-core rate with no memory traffic (measurement aid
+    libfp8probe.so): HIP events around each launch on the current stream."""
+    import ctypes
+    import torch
+    path = os.path.join(ROOT, "paper_2309_17224_amd", "libfp8probe.so")
+    if not os.path.exists(path):
+        raise SystemExit(f"{path} is missing: build it with `python -m paper_2309_17224_amd.build`")
+    P = ctypes.CDLL(path)
+    P.fp8probe_mfma_loop.restype = ctypes.c_int32
+    P.fp8probe_mfma_loop.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    P.fp8probe_mfma_loop_flops.restype = ctypes.c_int64
+    P.fp8probe_mfma_loop_flops.argtypes = [ctypes.c_int32, ctypes.c_int32]
+    blocks, iters = torch.cuda.get_device_properties(0).multi_processor_count, args.mfma_ceiling
+    out = torch.zeros(blocks * 8, dtype=torch.float32, device="cuda")
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    flops = P.fp8probe_mfma_loop_flops(blocks, iters)
+    ts = []
+    for i in range(max(args.warmup, 1) + args.steps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        if P.fp8probe_mfma_loop(blocks, iters, ctypes.c_void_p(out.data_ptr()), stream) != 0:
+            raise SystemExit("fp8probe_mfma_loop failed")
+        b.record()
+        torch.cuda.synchronize()
+        if i >= max(args.warmup, 1):
+            ts.append(a.elapsed_time(b) * 1e-3)
+    med = sorted(ts)[len(ts) // 2]
+    print(json.dumps({"mfma_loop": {"workgroups": blocks, "waves_per_workgroup": 8, "iters": iters,
+                                    "flop_per_launch": flops, "median_s": med,
+                                    "TFLOP_per_s": flops / med / 1e12,
+                                    "frac_of_fp8_peak": flops / med / 1e12 / FP8_PEAK_TFLOPS,
+                                    "launches": len(ts)}}), flush=True)
+
+
+def main(argv=None):
+    args = parse(argv)
     if args.gpus != 1:
-        print(json.dumps({"error": "bench.py measures one GPU only; --gpus %d is not supported"
-                          % args.gpus}))
+        print(json.dumps({"error": "bench.py measures one GPU only; --gpus %d is not supported: the "
+                                   "path shards with no FP8-specific exchange (see the design notes), "
+                                   "and this build measures the one-GPU share" % args.gpus}))
         sys.exit(2)
     import torch
     from paper_2309_17224_amd import fp8lin
-    from paper_2309_17224_amd import linear as L
     from paper_2309_17224_amd import workloads as wl
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a GPU")
@@ -385,6 +585,9 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes_per_launch": nbytes, "launches": args.steps}))
+        return
+    if args.mfma_ceiling:
+        mfma_ceiling(args)
         return
     fp8lin.lib()  # fails loudly when the HIP library is missing
     if args.amax_mb:
@@ -411,57 +614,27 @@ def main():
         bench_layer(args, wl.LAYERS[args.workload])
         return
     w = wl.WORKLOADS[args.workload]
-    dev = torch.device("cuda:0")
-    cpu = make_inputs(w)
-    tens = {k: v.to(dev) for k, v in cpu.items()}
-    torch.cuda.synchronize()
-    step = L.WorkloadStep(w, tens, dev, margin=args.margin, quant=args.quant,
-                          cscale_bias=args.cscale_bias, fused_bias=args.bias == "fused",
-                          concurrent=args.streams == 2, batch_quant=not args.no_quant_batch)
-    if not w.train:
-        step.prepare_inference()
-    flush = None
-    if args.flush_mb:
-        flush = torch.zeros(args.flush_mb * (1 << 20) // 4, dtype=torch.float32, device=dev)
-    log(f"[bench] {w.name}: {len(step.calls)} calls per step; warmup {args.warmup}, steps {args.steps}")
-    # eager pass: every call bracketed by HIP events on its stream (roofline table)
-    wall, per_call, flush_s = time_steps(step, args.steps, args.warmup, flush)
-    eager_step_s = (wall - flush_s) / args.steps
-    step_s = eager_step_s
-    if args.launch == "graph":
-        gwall, gflush = time_graph(step, args.steps, args.warmup, flush)
-        step_s = (gwall - gflush) / args.steps
-    flops = step.gemm_flops()
-    value = flops / step_s / 1e12
-    roof, table = roofline(step, per_call)
-    roof["traffic"] = measured_traffic(w.name, roof["kernel"])
-    for kind, d in sorted(table.items()):
-        log(f"[bench] {kind:9s} " + " ".join(f"{k}={v:.4g}" if isinstance(v, float) else f"{k}={v}"
-                                             for k, v in d.items()))
-    out = {
-        "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_s * 1e3, 4),
-        "eager_ms_per_step": round(eager_step_s * 1e3, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "fp8",
-        "data": "synthetic",
-        "config": {"workload": w.name, "description": w.description,
-                   "linears": [dict(name=l.name, M=l.M, K=l.K, N=l.N) for l in w.linears],
-                   "mode": "train fwd+bwd" if w.train else "PTQ inference fwd",
-                   "accumulate": "fp32", "outputs": "Y,dX bf16; dW fp32",
-                   "margin": args.margin, "mall_flush_mb": args.flush_mb, "quant": args.quant, "quant_batch": not args.no_quant_batch,
-                   "output_bias": args.bias,
-                   "launch": (f"one HIP graph replay per step, {args.streams} stream(s)" if args.launch == "graph"
-                              else "one host call per library call")},
-        "frac_of_fp8_peak": round(value / FP8_PEAK_TFLOPS, 4),
-        "roofline": roof,
-        "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv) for kk, vv in d.items()}
-                    for k, d in table.items()},
-    }
-    if not args.no_cpu_baseline:
-        log("[bench] timing the CPU oracle on a bounded sample")
-        out["cpu_baseline"] = cpu_baseline(w, cpu, args.cpu_budget)
-    else:
-        out["cpu_baseline"] = None
+    res = bench_workload(args, w, args.steps, args.warmup,
+                         cpu_baseline_budget=None if args.no_cpu_baseline else args.cpu_budget,
+                         mispredicted=not args.no_mispredicted)
+    out = {"metric": METRIC, "value": res.pop("value"), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": res.pop("ms_per_step"),
+           "eager_ms_per_step": res.pop("eager_ms_per_step"), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "fp8", "data": "synthetic", "config": res.pop("config")}
+    out.update(res)
+    out.setdefault("cpu_baseline", None)
+    if not args.no_configs and args.workload == DEFAULT_WORKLOAD:
+        side = {}
+        for name in SIDE_WORKLOADS:
+            r = bench_workload(args, wl.WORKLOADS[name], args.side_steps, min(args.warmup, 5))
+            side[name] = {"value": r["value"], "unit": "TFLOP/s", "ms_per_step": r["ms_per_step"],
+                          "frac_of_fp8_peak": r["frac_of_fp8_peak"], "steps": args.side_steps,
+                          "description": r["config"]["description"],
+                          "inputs_sha256": r["config"]["inputs_sha256"],
+                          "roofline": r["roofline"],
+                          "kernels": {k: {kk: v[kk] for kk in ("achieved", "unit", "frac", "avg_us")
+                                          if kk in v} for k, v in r["kernels"].items()}}
+        out["configs"] = side
     print(json.dumps(out), flush=True)
 
 

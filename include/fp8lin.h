@@ -106,7 +106,9 @@ size_t fp8_scale_bias_ws_bytes(int64_t n);
  * margin:    subtracted from the bias (Sec. 3.2: 3 was used with FP16
  *            accumulation; 0 with fp32 accumulation).  |margin| <= FP8_MAX_MARGIN.
  * bias:      out, one int32 (device).
- * amax_bits: out, optional: the fp32 bit pattern of the amax (device).
+ * amax_bits: out, optional: the fp32 bit pattern of the amax (device); a
+ *            tensor holding a NaN has amax 0x7FC00000, whatever the NaN
+ *            payloads.
  * flags:     out, optional: see the conventions above (device).
  * ws:        device workspace of at least fp8_scale_bias_ws_bytes(n) bytes,
  *            4-byte aligned; its contents are scratch.  Concurrent calls need
@@ -175,6 +177,9 @@ int32_t fp8_cast(const void *x, int32_t dt, int64_t rows, int64_t cols, int64_t 
  * bias, amax_bits, flags: out, as fp8_scale_bias (amax_bits, flags optional).
  * ws:        device workspace of at least fp8_quantise_ws_bytes(rows, cols)
  *            bytes, 4-byte aligned; scratch, distinct for concurrent calls.
+ *            (fp8_quantise_ws_bytes is SIZE_MAX for a tensor of more than
+ *            INT32_MAX tiles of 128 x 128, which fp8_quantise rejects with
+ *            FP8_ENOTSUP.)
  * rows == 0 or cols == 0 gives amax 0, bias 0 and FP8_FLAG_ZERO, no codes.
  */
 size_t fp8_quantise_ws_bytes(int64_t rows, int64_t cols);
@@ -269,9 +274,17 @@ int32_t fp8_bias_mode(const int32_t *bias, int64_t n, int32_t *ring, int64_t cap
  * y:   out, [M, N] dense, y_dt = FP8_DT_BF16 or FP8_DT_F32.
  * y_amax_bits: optional out: if given, the fp32 bit pattern of max|Y| (of
  *      the rounded outputs) is written there, so that the next layer can take
- *      its bias with fp8_bias_from_amax instead of reading Y again.
- * M == 0 or N == 0 is a no-op; K == 0 writes zeros.
- * Pointers must be 16-byte aligned.
+ *      its bias with fp8_bias_from_amax instead of reading Y again.  A NaN
+ *      output gives 0x7FC00000.
+ * M == 0 or N == 0: nothing is computed and *y_amax_bits (if given) is set to
+ * 0, the amax of an empty output; K == 0 writes zeros.
+ * Alignment: x8 and w8t must start on 16-byte boundaries whatever K is, y on
+ * its element size; FP8_EINVAL otherwise.
+ * Kernels: K a multiple of 128 runs the matrix-core kernels that stage whole
+ * 128-byte rows of both operands through LDS; any other K runs a 64 x 64 tile
+ * kernel that loads single bytes with bounds checks: the same results, about
+ * 3x the time of the staged kernels on large shapes.
+ * The same rules hold for every matmul entry point below.
  */
 int32_t fp8_linear_fwd(const uint8_t *x8, const int32_t *bx, const uint8_t *w8t, const int32_t *bw,
                        void *y, int32_t y_dt, int64_t M, int64_t N, int64_t K,

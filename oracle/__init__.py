@@ -18,6 +18,9 @@ Paper passages (section / equation / table):
     tensor replica (Sec. 4) and per data sample at inference (App. D): each
     row segment is an independent tensor for ``scale_bias`` and ``cast``
   * ``bias_mode``: the statistical mode of per-sample biases (App. D, App. F)
+  * ``quantise_delayed``: delayed scaling, the amax-history remedy Sec. 3 cites
+    for the second pass over a tensor: the bias of a call is Eq. 3 of the
+    largest amax recorded by the previous calls, used as it is
   * ``oracle.decoder``: the higher-precision glue of the Llama 2 decoder layer
     (RMSNorm, RoPE, causal grouped-query attention, SwiGLU, residual adds)
     around its four FP8 linears (App. E), and the layer as a chain (numpy, fp64)
@@ -247,6 +250,65 @@ def bias_mode(biases) -> int:
         counts[v] = counts.get(v, 0) + 1
     top = max(counts.values())
     return min(v for v, c in counts.items() if c == top)
+
+
+FLAG_SATURATED = 4
+
+
+def _f32(bits: int) -> float:
+    return float(np.array([bits], dtype=np.uint32).view(np.float32)[0])
+
+
+def history_max(history) -> int:
+    """The largest of a list of amax values given as fp32 bit patterns (sign
+    clear): the pattern of the largest value, or the canonical NaN 0x7FC00000
+    when one of them is NaN.  An empty list gives 0."""
+    vals = [_f32(h) for h in history]
+    if any(np.isnan(v) for v in vals):
+        return 0x7FC00000
+    if not vals:
+        return 0
+    best = max(range(len(vals)), key=lambda i: vals[i])
+    return int(history[best])
+
+
+def quantise_delayed(xs, fmt: int, margin: int = 0, history_len: int = 16, bias0: int = 0):
+    """Delayed scaling over a sequence of tensors (one call each).
+
+    Call t casts its tensor with bias b_t, computed before the tensor is read:
+    b_0 = bias0, and b_{t+1} is Eq. 3 (minus the margin) of the largest amax
+    among the last history_len calls (calls 0..t); the history starts as
+    history_len zeros.  So each tensor is read once: its own amax only enters
+    the biases of later calls.  When a tensor's amax * 2^b_t exceeds the
+    format's largest value its codes clip (App. A) and the call reports
+    FLAG_SATURATED.  Flags otherwise describe the tensor's own amax (NaN or
+    infinite: FLAG_NONFINITE; zero: FLAG_ZERO).
+
+    Returns a list of dicts per call: q (codes), bias (b_t), amax (bit
+    pattern of the tensor's amax), flags, next_bias (b_{t+1}); and the final
+    history (list of bit patterns, slot t % history_len written by call t).
+    """
+    if history_len < 1:
+        raise ValueError("history_len must be at least 1")
+    hist = [0] * history_len
+    b = int(bias0)
+    out = []
+    mx = max_num(fmt)
+    for t, x in enumerate(xs):
+        q = cast(x, fmt, b)
+        a = amax_bits(x)
+        av = _f32(a)
+        if np.isnan(av) or np.isinf(av):
+            fl = FLAG_NONFINITE
+        elif av == 0.0:
+            fl = FLAG_ZERO
+        else:
+            fl = FLAG_SATURATED if av * 2.0 ** b > mx else 0
+        hist[t % history_len] = a
+        nb, _ = bias_from_amax(history_max(hist), fmt, margin)
+        out.append(dict(q=q, bias=b, amax=a, flags=fl, next_bias=nb))
+        b = nb
+    return out, hist
 
 
 def bf16_to_f64(h: int) -> float:

@@ -15,6 +15,9 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libfp8lin.so")
 SOURCES = ["fp8lin_api.hip", "fp8lin_amax_cast.hip", "fp8lin_gemm.hip", "fp8lin_decoder.hip"]
+# measurement aid beside the library (bench.py --mfma-ceiling), not the method
+PROBE_LIB = os.path.join(PKG, "libfp8probe.so")
+PROBE_SOURCE = "fp8probe.hip"
 ARCH = "gfx950"
 
 
@@ -34,18 +37,23 @@ def flags() -> list[str]:
     ]
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source and link libfp8lin.so next to this file."""
-    objs = []
+def build(verbose: bool = False, jobs: int | None = None) -> str:
+    """Compile every source (in parallel) and link libfp8lin.so next to this file."""
+    from concurrent.futures import ThreadPoolExecutor
     obj_dir = os.path.join(PKG, "_build")
     os.makedirs(obj_dir, exist_ok=True)
-    for src in SOURCES:
-        obj = os.path.join(obj_dir, src.replace(".hip", ".o"))
-        cmd = [hipcc()] + flags() + ["-c", os.path.join(CSRC, src), "-o", obj]
-        if verbose:
+    objs = [os.path.join(obj_dir, src.replace(".hip", ".o")) for src in SOURCES]
+    cmds = [[hipcc()] + flags() + ["-c", os.path.join(CSRC, src), "-o", obj] for src, obj in zip(SOURCES, objs)]
+    probe_tmp = PROBE_LIB + ".tmp%d" % os.getpid()
+    cmds.append([hipcc()] + flags() + ["-shared", os.path.join(CSRC, PROBE_SOURCE), "-o", probe_tmp])
+    if verbose:
+        for cmd in cmds:
             print(" ".join(cmd), flush=True)
-        subprocess.run(cmd, check=True)
-        objs.append(obj)
+    jobs = jobs or min(len(cmds), max(1, (os.cpu_count() or 1) // 2))
+    with ThreadPoolExecutor(max_workers=jobs) as ex:
+        for r in ex.map(lambda c: subprocess.run(c, check=True), cmds):
+            pass
+    os.replace(probe_tmp, PROBE_LIB)
     tmp = LIB + ".tmp%d" % os.getpid()
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs
     if verbose:

@@ -97,7 +97,7 @@ __global__ __launch_bounds__(kAmaxThreads) void amax_finalize_kernel(
     uint32_t m = strided_max<kAmaxThreads>(partial, nparts);
     m = block_max(m, red);
     if (threadIdx.x == 0) {
-        const uint32_t a32 = DT == FP8_DT_BF16 ? (m << 16) : m;
+        const uint32_t a32 = canon_amax(DT == FP8_DT_BF16 ? (m << 16) : m);
         uint32_t fl;
         const int32_t b = bias_of<FMT>(a32, margin, &fl);
         *bias = b;
@@ -315,7 +315,7 @@ __device__ __forceinline__ void quant_pass2_body(
     m = block_max(m, red);
     if (threadIdx.x == 0) amax_s = m;
     __syncthreads();
-    const uint32_t a32 = DT == FP8_DT_BF16 ? (amax_s << 16) : amax_s;
+    const uint32_t a32 = canon_amax(DT == FP8_DT_BF16 ? (amax_s << 16) : amax_s);
     uint32_t fl;
     const int32_t bx = bias_of<FMT>(a32, margin, &fl);
     if (bid == 0 && threadIdx.x == 0) {
@@ -591,13 +591,13 @@ __global__ __launch_bounds__(kSegThreads) void seg_amax_kernel(const void* __res
         for (int i = 0; i < n; ++i) {
             const int si = seg_of(off, nseg, rb + i);
             if (si != s) {
-                atomicMax(amax + s, DT == FP8_DT_BF16 ? run << 16 : run);
+                atomicMax(amax + s, canon_amax(DT == FP8_DT_BF16 ? run << 16 : run));
                 s = si;
                 run = 0;
             }
             run = max(run, rmax[i]);
         }
-        if (n > 0) atomicMax(amax + s, DT == FP8_DT_BF16 ? run << 16 : run);
+        if (n > 0) atomicMax(amax + s, canon_amax(DT == FP8_DT_BF16 ? run << 16 : run));
     }
 }
 
@@ -747,6 +747,13 @@ int32_t launch_quant_check(const void* x, int dt, int64_t rows, int64_t cols, in
 int64_t quantise_ws_words(int64_t rows, int64_t cols) {
     const int64_t tiles = ((rows + kCastRows - 1) / kCastRows) * ((cols + kCastCols - 1) / kCastCols);
     return 1 + tiles;
+}
+
+int64_t quantise_tiles_upto(int64_t rows, int64_t cols, int64_t limit) {
+    const int64_t tr = (rows + kCastRows - 1) / kCastRows, tc = (cols + kCastCols - 1) / kCastCols;
+    if (tr == 0 || tc == 0) return 0;
+    if (tr > limit / tc) return -1;
+    return tr * tc;
 }
 
 int32_t launch_quantise(const void* x, int dt, int64_t rows, int64_t cols, int64_t ldx, int fmt,

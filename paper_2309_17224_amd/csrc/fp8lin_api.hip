@@ -27,15 +27,20 @@ int32_t cast_common(const void* x, int32_t dt, int64_t rows, int64_t cols, int64
     return launch_cast(x, dt, rows, cols, ldx, fmt, bias, q, ldq, qT, ldqT, as_stream(stream));
 }
 
+// Matmul operands (FP8 codes) start on 16-byte boundaries when K > 0.
+bool operands_ok(const uint8_t* a, const uint8_t* b, int64_t K) { return K == 0 || (a16(a) && a16(b)); }
+
 int32_t gemm_common(const uint8_t* a, int fa, const int32_t* ba, const uint8_t* b, int fb,
                     const int32_t* bb, void* c, int32_t c_dt, int64_t M, int64_t N, int64_t K,
                     uint32_t* amax, void* stream) {
     if (!dt_ok(c_dt) || M < 0 || N < 0 || K < 0 || M > kMaxDim || N > kMaxDim || K > kMaxDim)
         return FP8_EINVAL;
-    if (M == 0 || N == 0) return FP8_OK;
+    if (amax && !aligned(amax, 4)) return FP8_EINVAL;
+    if (M == 0 || N == 0)  // no output: its amax is 0
+        return amax ? launch_fill_u32(amax, 0u, as_stream(stream)) : FP8_OK;
     if (!c || !ba || !bb || (K > 0 && (!a || !b))) return FP8_EINVAL;
     if (!aligned(c, esize(c_dt)) || !aligned(ba, 4) || !aligned(bb, 4)) return FP8_EINVAL;
-    if (amax && !aligned(amax, 4)) return FP8_EINVAL;
+    if (!operands_ok(a, b, K)) return FP8_EINVAL;
     if (M > INT32_MAX || N > INT32_MAX) return FP8_ENOTSUP;
     return launch_gemm_nt(a, fa, ba, b, fb, bb, c, c_dt, M, N, K, amax, as_stream(stream));
 }
@@ -124,27 +129,50 @@ int32_t fp8_cast(const void* x, int32_t dt, int64_t rows, int64_t cols, int64_t 
 
 size_t fp8_quantise_ws_bytes(int64_t rows, int64_t cols) {
     if (rows <= 0 || cols <= 0 || rows > kMaxDim || cols > kMaxDim) return 0;
+    if (quantise_tiles_upto(rows, cols, INT32_MAX) < 0) return SIZE_MAX;  // beyond what a call accepts
     return (size_t)quantise_ws_words(rows, cols) * sizeof(uint32_t);
 }
 
-int32_t fp8_quantise(const void* x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx,
-                     int32_t fmt, int32_t margin, const int32_t* bias_pred, int32_t* bias,
-                     uint32_t* amax_bits, uint32_t* flags, uint8_t* q, int64_t ldq, uint8_t* qT,
-                     int64_t ldqT, void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+// Checks of fp8_quantise's arguments other than the workspace; *empty is set
+// when there is nothing to cast (rows == 0 or cols == 0).
+int32_t quantise_checks(const void* x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx, int32_t fmt,
+                        int32_t margin, const int32_t* bias_pred, int32_t* bias, uint32_t* amax_bits,
+                        uint32_t* flags, uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT, bool* empty) {
+    *empty = false;
     if (!dt_ok(dt) || !fmt_ok(fmt) || rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim)
         return FP8_EINVAL;
     if (margin > FP8_MAX_MARGIN || margin < -FP8_MAX_MARGIN) return FP8_EINVAL;
     if (!bias || !aligned(bias, 4)) return FP8_EINVAL;
     if ((amax_bits && !aligned(amax_bits, 4)) || (flags && !aligned(flags, 4))) return FP8_EINVAL;
     if (bias_pred && !aligned(bias_pred, 4)) return FP8_EINVAL;
-    if (rows == 0 || cols == 0)  // amax 0: bias 0 and the zero flag, nothing to cast
-        return launch_scale_bias(x, dt, 0, fmt, margin, bias, amax_bits, flags, nullptr,
-                                 as_stream(stream));
-    if (!x || (!q && !qT) || !ws) return FP8_EINVAL;
-    if (!aligned(x, esize(dt)) || !aligned(ws, 4)) return FP8_EINVAL;
+    if (rows == 0 || cols == 0) {
+        *empty = true;
+        return FP8_OK;
+    }
+    if (!x || (!q && !qT)) return FP8_EINVAL;
+    if (!aligned(x, esize(dt))) return FP8_EINVAL;
     if (ldx < cols || (q && ldq < cols) || (qT && ldqT < rows)) return FP8_EINVAL;
-    if (ws_bytes < fp8_quantise_ws_bytes(rows, cols)) return FP8_EINVAL;
-    if (quantise_ws_words(rows, cols) - 1 > INT32_MAX) return FP8_ENOTSUP;
+    if (quantise_tiles_upto(rows, cols, INT32_MAX) < 0) return FP8_ENOTSUP;
+    return FP8_OK;
+}
+}  // namespace
+
+extern "C" {
+
+int32_t fp8_quantise(const void* x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx,
+                     int32_t fmt, int32_t margin, const int32_t* bias_pred, int32_t* bias,
+                     uint32_t* amax_bits, uint32_t* flags, uint8_t* q, int64_t ldq, uint8_t* qT,
+                     int64_t ldqT, void* ws, size_t ws_bytes, void* stream) {
+    bool empty;
+    const int32_t st = quantise_checks(x, dt, rows, cols, ldx, fmt, margin, bias_pred, bias, amax_bits, flags, q,
+                                       ldq, qT, ldqT, &empty);
+    if (st != FP8_OK) return st;
+    if (empty)  // amax 0: bias 0 and the zero flag, nothing to cast
+        return launch_scale_bias(x, dt, 0, fmt, margin, bias, amax_bits, flags, nullptr, as_stream(stream));
+    if (!ws || !aligned(ws, 4) || ws_bytes < fp8_quantise_ws_bytes(rows, cols)) return FP8_EINVAL;
     return launch_quantise(x, dt, rows, cols, ldx, fmt, margin, bias_pred, bias, amax_bits, flags,
                            q, ldq, qT, ldqT, (uint32_t*)ws, as_stream(stream));
 }
@@ -168,8 +196,9 @@ int32_t fp8_quantise_batch(int32_t n, const fp8_quantise_args* t, int32_t dt, in
         if (!aligned(a.x, esize(dt)) || !aligned(a.ws, 4)) return FP8_EINVAL;
         if (a.ldx < a.cols || (a.q && a.ldq < a.cols) || (a.qT && a.ldqT < a.rows)) return FP8_EINVAL;
         if (a.ws_bytes < fp8_quantise_ws_bytes(a.rows, a.cols)) return FP8_EINVAL;
-        if (quantise_ws_words(a.rows, a.cols) - 1 > INT32_MAX) return FP8_ENOTSUP;
-        tiles += quantise_ws_words(a.rows, a.cols) - 1;
+        const int64_t nt = quantise_tiles_upto(a.rows, a.cols, INT32_MAX);
+        if (nt < 0) return FP8_ENOTSUP;
+        tiles += nt;
         npred += a.bias_pred ? 1 : 0;
         d[m++] = QuantDesc{a.x, a.rows, a.cols, a.ldx, a.bias_pred, a.bias, a.amax_bits, a.flags,
                            a.q, a.ldq, a.qT, a.ldqT, (uint32_t*)a.ws};
@@ -248,6 +277,7 @@ int32_t gemm_bias_common(const uint8_t* a, int fa, const int32_t* ba, const uint
                                  as_stream(stream));
     if (!c || !ba || !bb || (kc > 0 && (!a || !b))) return FP8_EINVAL;
     if (!aligned(c, esize(c_dt)) || !aligned(ba, 4) || !aligned(bb, 4)) return FP8_EINVAL;
+    if (!operands_ok(a, b, kc)) return FP8_EINVAL;
     if (rows > INT32_MAX || cols > INT32_MAX) return FP8_ENOTSUP;
     return launch_gemm_nt_bias(a, fa, ba, b, fb, bb, c, c_dt, rows, cols, kc, fmt, margin, bias, amax_bits, flags,
                                (uint32_t*)ws, as_stream(stream));
@@ -294,6 +324,7 @@ int32_t gemm_quantise_common(const uint8_t* a, int fa, const int32_t* ba, const 
                                  as_stream(stream));
     if (!c || !ba || !bb || !q || (kc > 0 && (!a || !b)) || !ws) return FP8_EINVAL;
     if (!aligned(c, 2) || !aligned(ba, 4) || !aligned(bb, 4) || !aligned(ws, 4)) return FP8_EINVAL;
+    if (!operands_ok(a, b, kc)) return FP8_EINVAL;
     if (ldq < cols || (qT && ldqT < rows)) return FP8_EINVAL;
     if (ws_bytes < fp8_linear_quantise_ws_bytes(rows, cols)) return FP8_EINVAL;
     if (rows > INT32_MAX || cols > INT32_MAX) return FP8_ENOTSUP;
@@ -348,10 +379,12 @@ int32_t fp8_linear_fwd_rows(const uint8_t* x8, const int32_t* bx_rows, const uin
                             void* y, int32_t y_dt, int64_t M, int64_t N, int64_t K, uint32_t* y_amax_bits,
                             void* stream) {
     if (!dt_ok(y_dt) || M < 0 || N < 0 || K < 0 || M > kMaxDim || N > kMaxDim || K > kMaxDim) return FP8_EINVAL;
-    if (M == 0 || N == 0) return FP8_OK;
+    if (y_amax_bits && !aligned(y_amax_bits, 4)) return FP8_EINVAL;
+    if (M == 0 || N == 0)  // no output: its amax is 0
+        return y_amax_bits ? launch_fill_u32(y_amax_bits, 0u, as_stream(stream)) : FP8_OK;
     if (!y || !bx_rows || !bw || (K > 0 && (!x8 || !w8t))) return FP8_EINVAL;
     if (!aligned(y, esize(y_dt)) || !aligned(bx_rows, 4) || !aligned(bw, 4)) return FP8_EINVAL;
-    if (y_amax_bits && !aligned(y_amax_bits, 4)) return FP8_EINVAL;
+    if (!operands_ok(x8, w8t, K)) return FP8_EINVAL;
     if (M > INT32_MAX || N > INT32_MAX) return FP8_ENOTSUP;
     return launch_gemm_nt(x8, FP8_E4M3, bx_rows, w8t, FP8_E4M3, bw, y, y_dt, M, N, K, y_amax_bits,
                           as_stream(stream), 1);

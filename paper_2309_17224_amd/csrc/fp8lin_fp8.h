@@ -76,6 +76,14 @@ __device__ __forceinline__ int32_t bias_of(uint32_t u, int32_t margin, uint32_t*
 }
 
 // ---------------------------------------------------------------- amax
+// The amax of a tensor holding a NaN is NaN; its fp32 pattern is the canonical
+// quiet NaN 0x7FC00000 whatever the payloads of the input NaNs.  Mapping every
+// contribution before it is folded into a maximum keeps the fold exact: the
+// canonical NaN pattern exceeds every finite or infinite magnitude pattern.
+__device__ __forceinline__ uint32_t canon_amax(uint32_t a32) {
+    return a32 > 0x7F800000u ? 0x7FC00000u : a32;
+}
+
 typedef unsigned short us2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ uint32_t wave_max(uint32_t v) {

@@ -552,12 +552,13 @@ __device__ __forceinline__ void gemm_tile(
             uint32_t b = 0;
 #pragma unroll
             for (int v = 0; v < kMainThreads / 64; ++v) b = max(b, wmx[v]);
-            if (AMAX && !bo.ws) atomicMax(amax_out, b);
+            const uint32_t bc = canon_amax(b);  // the fold and the atomics take canonical NaNs
+            if (AMAX && !bo.ws) atomicMax(amax_out, bc);
             if (AMAX && bo.ws) {
                 // The fold returns its old value, which is consumed before the
                 // count is issued, so the fold has been performed by then; the
                 // workgroup that counts last therefore sees every fold.
-                const uint32_t prev = __hip_atomic_fetch_max(bo.ws, b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                const uint32_t prev = __hip_atomic_fetch_max(bo.ws, bc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 asm volatile("; fold returned %0" : : "v"(prev));
                 const uint32_t done = __hip_atomic_fetch_add(bo.ws + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 if (done == gridDim.x - 1) {
@@ -675,7 +676,7 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_small(
     }
     if (AMAX) {
         mx = wave_max_u32(mx);
-        if (lane == 0) atomicMax(amax_out, mx);
+        if (lane == 0) atomicMax(amax_out, canon_amax(mx));
     }
 }
 
@@ -780,7 +781,7 @@ __global__ __launch_bounds__(kDecWaves * 64) void gemm_nt_decode(
     }
     if (AMAX) {
         mx = wave_max_u32(mx);
-        if (lane == 0) atomicMax(amax_out, mx);
+        if (lane == 0) atomicMax(amax_out, canon_amax(mx));
     }
 }
 
@@ -870,7 +871,7 @@ __global__ __launch_bounds__(256) void gemm_nt_decode_lds(
     }
     if (AMAX) {
         mx = wave_max_u32(mx);
-        if (lane == 0) atomicMax(amax_out, mx);
+        if (lane == 0) atomicMax(amax_out, canon_amax(mx));
     }
 }
 
@@ -1061,6 +1062,11 @@ int32_t launch_gemm_nt_quantise(const uint8_t* A, int fa, const int32_t* ba, con
     if (st != FP8_OK) return st;
     return launch_quant_check(C, FP8_DT_BF16, M, N, N, qfmt, margin, ws + 1, tiles, (int32_t*)ws, bias, amax_bits,
                               flags, y8, ldy8, y8t, ldy8t, s);
+}
+
+int32_t launch_fill_u32(uint32_t* p, uint32_t v, hipStream_t s) {
+    hipLaunchKernelGGL(fill_u32_kernel, dim3(1), dim3(64), 0, s, p, v);
+    return hip_status();
 }
 
 int32_t launch_gemm_nt(const uint8_t* A, int fa, const int32_t* ba, const uint8_t* B, int fb,

@@ -28,6 +28,9 @@ int32_t launch_cast(const void* x, int dt, int64_t rows, int64_t cols, int64_t l
 // amax + bias + cast of a rows x cols tensor (two kernels); ws holds
 // quantise_ws_words(rows, cols) uint32 words.
 int64_t quantise_ws_words(int64_t rows, int64_t cols);
+// Number of quantise tiles of a rows x cols tensor, or -1 when it exceeds
+// limit (computed without overflow for any sizes below 2^62).
+int64_t quantise_tiles_upto(int64_t rows, int64_t cols, int64_t limit);
 
 // fp8_quantise of several tensors of one type and format (checked arguments).
 constexpr int kQBatch = FP8_QUANTISE_BATCH_MAX;
@@ -129,6 +132,9 @@ int32_t launch_swiglu(const uint16_t* gu, int64_t ldgu, int64_t rows, int64_t ff
                       const FusedQuant* fq, hipStream_t s);
 int32_t launch_attention(const uint16_t* qkv, int64_t rows, int64_t ld, int64_t seq_len, int nh, int nkv,
                          uint16_t* o, int64_t ldo, const FusedQuant* fq, hipStream_t s);
+
+// *p = v on the stream (one word).
+int32_t launch_fill_u32(uint32_t* p, uint32_t v, hipStream_t s);
 
 inline int32_t hip_status() { return hipGetLastError() == hipSuccess ? FP8_OK : FP8_EHIP; }
 

@@ -201,7 +201,11 @@ class WorkloadStep:
 
     def __init__(self, workload, tensors: dict, device, margin: int = 0, quant: str = "predicted",
                  cscale_bias: int = 0, fused_bias: bool = True, concurrent: bool = False,
-                 batch_quant: bool = True):
+                 batch_quant: bool = True, share: "WorkloadStep | None" = None):
+        """share: another step of the same workload whose FP8 buffers, biases
+        and outputs this one uses (its own input tensors only): steps over two
+        input sets that write one set of codes, each taking its bias
+        predictions from the other's last step."""
         if quant not in self.QUANT_MODES:
             raise ValueError(f"quant must be one of {self.QUANT_MODES}")
         self.fused_bias = bool(fused_bias)
@@ -212,84 +216,134 @@ class WorkloadStep:
         self.quant = quant
         self.cscale_bias = int(cscale_bias)
         lin = workload.linears
-        nmax = max(x.numel() for x in tensors.values())
-        self.ws = F.workspace(nmax, device)
-        self.q = {}
         train = workload.train
-        for l in lin:
-            K, N, M = l.K, l.N, l.M
-            if l.w not in self.q:
-                self.q[l.w] = Fp8Tensor(K, N, device, want_q=train, want_qT=True)
-            if l.x not in self.q:
-                self.q[l.x] = Fp8Tensor(M, K, device, want_q=True, want_qT=train)
-            if train and l.dy not in self.q:
-                self.q[l.dy] = Fp8Tensor(M, N, device, want_q=True, want_qT=True)
-        self.out = {}
-        for l in lin:
-            o = dict(y=torch.empty((l.M, l.N), dtype=torch.bfloat16, device=device),
-                     y_scal=torch.zeros(3, dtype=torch.int32, device=device))
-            if train:
-                o.update(dx=torch.empty((l.M, l.K), dtype=torch.bfloat16, device=device),
-                         dw=torch.empty((l.K, l.N), dtype=torch.float32, device=device),
-                         dx_scal=torch.zeros(3, dtype=torch.int32, device=device))
-            self.out[l.name] = o
-        # bias workspaces of the forward and grad-input matmuls (zero between calls)
-        self.bws = {l.name: F.bias_workspace(device) for l in lin}
-        # a workspace per tensor: calls on different streams never share one
-        for name, qt in self.q.items():
-            x = tensors[name]
-            qt.qws = torch.empty(max(F.fp8_quantise_ws_bytes(*x.shape), 4), dtype=torch.uint8, device=device)
-            qt.sws = F.workspace(x.numel(), device)
+        if share is not None:
+            if share.w is not workload:
+                raise ValueError("a shared step must run the same workload")
+            self.ws, self.q, self.out, self.bws = share.ws, share.q, share.out, share.bws
+        else:
+            nmax = max(x.numel() for x in tensors.values())
+            self.ws = F.workspace(nmax, device)
+            self.q = {}
+            for l in lin:
+                K, N, M = l.K, l.N, l.M
+                if l.w not in self.q:
+                    self.q[l.w] = Fp8Tensor(K, N, device, want_q=train, want_qT=True)
+                if l.x not in self.q:
+                    self.q[l.x] = Fp8Tensor(M, K, device, want_q=True, want_qT=train)
+                if train and l.dy not in self.q:
+                    self.q[l.dy] = Fp8Tensor(M, N, device, want_q=True, want_qT=True)
+            self.out = {}
+            for l in lin:
+                o = dict(y=torch.empty((l.M, l.N), dtype=torch.bfloat16, device=device),
+                         y_scal=torch.zeros(3, dtype=torch.int32, device=device))
+                if train:
+                    o.update(dx=torch.empty((l.M, l.K), dtype=torch.bfloat16, device=device),
+                             dw=torch.empty((l.K, l.N), dtype=torch.float32, device=device),
+                             dx_scal=torch.zeros(3, dtype=torch.int32, device=device))
+                self.out[l.name] = o
+            # bias workspaces of the forward and grad-input matmuls (zero between calls)
+            self.bws = {l.name: F.bias_workspace(device) for l in lin}
+            # a workspace per tensor: calls on different streams never share one
+            for name, qt in self.q.items():
+                x = tensors[name]
+                qt.qws = torch.empty(max(F.fp8_quantise_ws_bytes(*x.shape), 4), dtype=torch.uint8, device=device)
+                qt.sws = F.workspace(x.numel(), device)
+        # transposed-code bytes each quantise / cast call writes beyond its
+        # algorithmic 3 bytes per element (layout overhead, reported apart)
+        self.layout_bytes = {}
         self.concurrent = bool(concurrent) and self.dev.type == "cuda"
         self.batch_quant = bool(batch_quant) and not self.concurrent and quant in ("predicted", "twopass")
         self.side = torch.cuda.Stream(self.dev) if self.concurrent else None  # default priority
         self.sched = []
         self.calls = self._build()
 
+    def _layout(self, name) -> int:
+        """Bytes of the second (transposed) copy of a tensor's codes."""
+        qt = self.q[name]
+        return self.t[name].numel() if qt.qT is not None and qt.q is not None else 0
+
     def _quant(self, name, fmt, margin):
+        """Work of a quantise or cast call: its algorithmic bytes, 2 read + 1
+        written per element; a transposed copy is layout overhead, recorded in
+        layout_bytes under the call's label."""
         x = self.t[name]
         qt = self.q[name]
         cast = F.fp8_cast_e4 if fmt == F.E4M3 else F.fp8_cast_e5
         n = x.numel()
-        code_bytes = n + (n if qt.qT is not None and qt.q is not None else 0)
         if self.quant == "cscale":
             qt.bias.fill_(self.cscale_bias)
-            return [(f"cast {name}", "cast", 2 * n + code_bytes,
+            self.layout_bytes[f"cast {name}"] = self._layout(name)
+            return [(f"cast {name}", "cast", 3 * n,
                      lambda: cast(x, qt.bias, q=qt.q, qT=qt.qT, want_q=qt.q is not None,
                                   want_qT=qt.qT is not None))]
         if self.quant != "separate":
             pred = qt.bias if self.quant == "predicted" else None
             # one read of the tensor and its codes when the prediction holds
-            return [(f"quantise {name}", "quantise", 2 * n + code_bytes,
+            self.layout_bytes[f"quantise {name}"] = self._layout(name)
+            return [(f"quantise {name}", "quantise", 3 * n,
                      lambda: F.fp8_quantise(x, fmt, margin, bias_pred=pred, bias=qt.bias,
                                             amax_bits=qt.amax, flags=qt.flags, q=qt.q, qT=qt.qT,
                                             want_q=qt.q is not None, want_qT=qt.qT is not None,
                                             ws=qt.qws))]
+        self.layout_bytes[f"cast {name}"] = self._layout(name)
         return [
             (f"amax+bias {name}", "amax", 2 * n,
              lambda: F.fp8_scale_bias(x, fmt, margin, bias=qt.bias, amax_bits=qt.amax,
                                       flags=qt.flags, ws=qt.sws)),
-            (f"cast {name}", "cast", 3 * n + (n if qt.qT is not None and qt.q is not None else 0),
+            (f"cast {name}", "cast", 3 * n,
              lambda: cast(x, qt.bias, q=qt.q, qT=qt.qT, want_q=qt.q is not None,
                           want_qT=qt.qT is not None)),
         ]
 
     def _quant_batch(self, names, fmt, margin):
         """The quantise calls of `names`, up to QUANTISE_BATCH_MAX tensors per
-        fp8_quantise_batch call."""
+        fp8_quantise_batch call (work counted as in _quant)."""
         calls = []
         for g in range(0, len(names), F.QUANTISE_BATCH_MAX):
             grp = names[g:g + F.QUANTISE_BATCH_MAX]
-            items, work = [], 0
+            items, work, layout = [], 0, 0
             for name in grp:
                 x, qt = self.t[name], self.q[name]
-                n = x.numel()
-                work += 2 * n + n + (n if qt.qT is not None and qt.q is not None else 0)
+                work += 3 * x.numel()
+                layout += self._layout(name)
                 items.append(dict(x=x, bias=qt.bias, bias_pred=qt.bias if self.quant == "predicted" else None,
                                   amax_bits=qt.amax, flags=qt.flags, q=qt.q, qT=qt.qT, ws=qt.qws))
-            calls.append((f"quantise {'+'.join(grp)}", "quantise", work,
+            label = f"quantise {'+'.join(grp)}"
+            self.layout_bytes[label] = layout
+            calls.append((label, "quantise", work,
                           lambda items=items: F.fp8_quantise_batch(items, fmt, margin)))
         return calls
+
+    def quantised(self):
+        """(name, format, margin) of every tensor the step quantises."""
+        out = {}
+        for l in self.w.linears:
+            out.setdefault(l.w, (F.E4M3, 0))
+            out.setdefault(l.x, (F.E4M3, 0))
+            if self.w.train:
+                out.setdefault(l.dy, (F.E5M2, self.margin))
+        return [(k, f, m) for k, (f, m) in out.items()]
+
+    def step_inputs(self):
+        """Names of the tensors every step quantises (inference weights are
+        quantised once beforehand, by prepare_inference)."""
+        names = [n for n, _, _ in self.quantised()]
+        if not self.w.train:
+            weights = {l.w for l in self.w.linears}
+            names = [n for n in names if n not in weights]
+        return names
+
+    def prediction_hits(self):
+        """(hits, tensors) of the last step's bias predictions ("predicted"
+        mode): a tensor's prediction held when the bias its codes were first
+        cast with (word 0 of its quantise workspace) is its exact bias."""
+        if self.quant != "predicted":
+            return 0, 0
+        names = self.step_inputs()
+        used = torch.stack([self.q[n].qws[:4].view(torch.int32)[0] for n in names]).cpu()
+        exact = torch.stack([self.q[n].bias[0] for n in names]).cpu()
+        return int((used == exact).sum()), len(names)
 
     def _build(self):
         """The step's calls in issue order; self.sched[i] = (phase, branch) of

@@ -51,6 +51,7 @@ def test_workspace_size(L):
 
 FAKE = ctypes.c_void_p(0x100000)       # aligned, never dereferenced: rejected before launch
 ODD = ctypes.c_void_p(0x100001)
+A8 = ctypes.c_void_p(0x100008)         # 8-byte but not 16-byte aligned
 NULL = None
 
 
@@ -124,10 +125,20 @@ def test_gemm_rejects(L):
         assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 0, -1, 4, 4, NULL, NULL) == F.EINVAL   # M < 0
         assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 0, 4, 4, 4, ODD, NULL) == F.EINVAL     # amax
         assert f(NULL, NULL, NULL, NULL, NULL, 0, 0, 4, 4, NULL, NULL) == F.OK        # empty
+        # FP8 operands must start on 16-byte boundaries (also where K is not a
+        # multiple of 128): rejected, not routed to another kernel
+        assert f(ODD, FAKE, FAKE, FAKE, FAKE, 0, 4, 4, 4, NULL, NULL) == F.EINVAL     # operand A
+        assert f(FAKE, FAKE, A8, FAKE, FAKE, 0, 4, 4, 4, NULL, NULL) == F.EINVAL      # operand B
+        assert f(FAKE, FAKE, A8, FAKE, FAKE, 0, 4, 4, 20, NULL, NULL) == F.EINVAL     # any K
     f = L.fp8_linear_bwd_dw
     assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 2, 4, 4, 4, NULL) == F.EINVAL
     assert f(FAKE, FAKE, NULL, FAKE, FAKE, 0, 4, 4, 4, NULL) == F.EINVAL
+    assert f(A8, FAKE, FAKE, FAKE, FAKE, 0, 4, 4, 4, NULL) == F.EINVAL
+    assert f(FAKE, FAKE, ODD, FAKE, FAKE, 0, 4, 4, 4, NULL) == F.EINVAL
     assert f(NULL, NULL, NULL, NULL, NULL, 0, 4, 0, 4, NULL) == F.OK
+    f = L.fp8_linear_fwd_rows
+    assert f(ODD, FAKE, FAKE, FAKE, FAKE, 0, 4, 4, 4, NULL, NULL) == F.EINVAL
+    assert f(FAKE, FAKE, A8, FAKE, FAKE, 0, 4, 4, 4, NULL, NULL) == F.EINVAL
 
 
 def test_ptq_and_bias_from_amax_reject(L):
@@ -155,6 +166,8 @@ def test_gemm_bias_rejects(L):
         assert f(FAKE, FAKE, FAKE, FAKE, NULL, 0, 4, 4, 4, 0, 0, FAKE, NULL, NULL, FAKE, 8, NULL) == F.EINVAL   # output
         assert f(FAKE, FAKE, FAKE, FAKE, ODD, 0, 4, 4, 4, 0, 0, FAKE, NULL, NULL, FAKE, 8, NULL) == F.EINVAL    # out align
         assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 0, -1, 4, 4, 0, 0, FAKE, NULL, NULL, FAKE, 8, NULL) == F.EINVAL  # M < 0
+        assert f(A8, FAKE, FAKE, FAKE, FAKE, 0, 4, 4, 4, 0, 0, FAKE, NULL, NULL, FAKE, 8, NULL) == F.EINVAL    # A align
+        assert f(FAKE, FAKE, ODD, FAKE, FAKE, 0, 4, 4, 4, 0, 0, FAKE, NULL, NULL, FAKE, 8, NULL) == F.EINVAL   # B align
 
 
 def test_segments_mode_rows_reject(L):

@@ -24,11 +24,7 @@ def gpu_bias(x_dev, fmt, margin=0):
 def check_bias(orc, x_cpu, fmt, dev, margin=0):
     ob, oa, ofl = orc.scale_bias(np_bits(x_cpu), fmt, margin)
     gb, ga, gfl = gpu_bias(x_cpu.to(dev), fmt, margin)
-    assert (gb, gfl) == (ob, ofl)
-    if (oa & 0x7F800000) == 0x7F800000 and (oa & 0x7FFFFF):
-        assert (ga & 0x7F800000) == 0x7F800000 and (ga & 0x7FFFFF)  # NaN: any payload
-    else:
-        assert ga == oa
+    assert (gb, gfl, ga) == (ob, ofl, oa)  # a NaN amax is 0x7FC00000 on both sides
     return gb
 
 

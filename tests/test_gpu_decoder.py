@@ -268,8 +268,9 @@ def test_rmsnorm_zero_and_nonfinite_rows(gpu, orc):
     assert np.array_equal(nan_g, nan_r)
     assert np.all(y[1] & 0x7FFF == 0)
     ulp_check(np.where(nan_g, 0, y).astype(np.uint16), np.where(nan_r, 0, y_ref).astype(np.uint16))
-    # the tensor holds NaN: the Eq. 3 bias is 0 with FLAG_NONFINITE, NaN codes are 0x7F with the sign
-    assert (i32(scal[0]), u32(scal[2])) == (0, F.FLAG_NONFINITE)
+    # the tensor holds NaN: the Eq. 3 bias is 0 with FLAG_NONFINITE, the amax the
+    # canonical NaN, NaN codes are 0x7F with the sign
+    assert (i32(scal[0]), u32(scal[1]), u32(scal[2])) == (0, 0x7FC00000, F.FLAG_NONFINITE)
     codes = fq.q.cpu().numpy()
     assert np.all(codes[nan_g] & 0x7F == 0x7F)
     q2, _, _, _, _ = F.fp8_quantise(bf16_dev(y, gpu), F.E4M3, 0)
@@ -289,4 +290,4 @@ def test_swiglu_nonfinite(gpu, orc):
     nan_g, nan_r = (a & 0x7FFF) > 0x7F80, (ref & 0x7FFF) > 0x7F80
     assert np.array_equal(nan_g, nan_r)
     assert np.array_equal(a[~nan_g] & 0x7FFF == 0x7F80, ref[~nan_r] & 0x7FFF == 0x7F80)   # same infinities
-    assert (i32(scal[0]), u32(scal[2])) == (0, F.FLAG_NONFINITE)
+    assert (i32(scal[0]), u32(scal[1]), u32(scal[2])) == (0, 0x7FC00000, F.FLAG_NONFINITE)

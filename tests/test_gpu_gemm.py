@@ -74,9 +74,10 @@ def test_gemm_scaled_normal_codes(orc, gpu, shape, entry, out_dt):
 # 16 products of a 16x16x128 instruction keeping about 13 significant bits
 # relative to the group's largest product (measured on gfx950: 65536 + 4 -> 65536
 # inside a group, exact across groups and across instructions, which add in
-# fp32).  Summed over groups this gives |err| <= 2^-13 sum_k |a_k b_k| per
-# output before the unscale; the test allows 2^-10.
-ELEM_BOUND = 2.0 ** -10
+# fp32).  Summed over groups this gives |err| of about 2^-13 sum_k |a_k b_k| per
+# output before the unscale; the largest ratio measured over these cases is
+# 2^-11.88 (forward, 255 x 1 x 17), and the test allows 2^-11.
+ELEM_BOUND = 2.0 ** -11
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "%dx%dx%d" % s)
@@ -96,6 +97,9 @@ def test_gemm_uniform_codes_elementwise_bound(orc, gpu, shape, entry):
     da, db = np.abs(orc.decode_table(fa)[A]), np.abs(orc.decode_table(fb)[B])
     absum = (da @ db.T) * 2.0 ** -(ba + bb)
     err = np.abs(got.astype(np.float64) - ref)
+    ratio = float((err / np.maximum(absum, 1e-300)).max()) if err.size else 0.0
+    print(f"\n[uniform codes] {entry} {shape}: max err/sum|ab| = 2^{np.log2(max(ratio, 1e-300)):.2f}, "
+          f"rel_F = {rel_f(got, ref.astype(np.float32)):.3e}", flush=True)
     assert (err <= ELEM_BOUND * absum + 1e-38).all()
 
 
@@ -145,12 +149,47 @@ def test_epilogue_amax(orc, gpu, out_dt):
     assert amax_dx == oa2
 
 
+# Shapes of the 256 x 256 kernel (with and without a narrow last round), the
+# decode kernels and the byte-load kernel (K not a multiple of 128).
+NAN_SHAPES = [(300, 520, 256), (512, 700, 384), (16, 640, 512), (24, 100, 256), (40, 90, 200)]
+
+
+@pytest.mark.parametrize("shape", NAN_SHAPES, ids=lambda s: "%dx%dx%d" % s)
+@pytest.mark.parametrize("out_dt", [F.DT_BF16, F.DT_F32], ids=["bf16", "f32"])
+def test_epilogue_amax_of_nan_output_is_canonical(orc, gpu, shape, out_dt):
+    """A NaN code in an operand makes outputs NaN; their amax, through the
+    epilogue atomics and through the in-launch bias, is 0x7FC00000 with
+    FP8_FLAG_NONFINITE and bias 0, the oracle's amax of a tensor holding NaN."""
+    M, N, K = shape
+    rng = np.random.default_rng(M + N + K)
+    A = rand_codes((M, K), 0, rng, orc)
+    B = rand_codes((N, K), 0, rng, orc)
+    A[M // 2, K // 3] = 0xFF            # E4M3 NaN (negative sign)
+    got, amax = run_nt("fwd", A, 0, 3, B, 0, 2, out_dt, gpu, M, N, K, amax=True)
+    assert amax == 0x7FC00000
+    ref_nan = orc.gemm_nt(A, 0, 3, B, 0, 2, out_dt=out_dt, rows=np.array([M // 2]))
+    assert orc.scale_bias(ref_nan, 0)[1] == 0x7FC00000
+    ta, tb = (torch.from_numpy(np.ascontiguousarray(v)).to(gpu) for v in (A, B))
+    pa = torch.tensor([3], dtype=torch.int32, device=gpu)
+    pb = torch.tensor([2], dtype=torch.int32, device=gpu)
+    _, b, a, fl = F.fp8_linear_fwd_bias(ta, pa, tb, pb, F.E4M3, 0, out_dt=out_dt)
+    torch.cuda.synchronize()
+    assert (i32(b), u32(a), u32(fl)) == (0, 0x7FC00000, F.FLAG_NONFINITE)
+
+
 def test_gemm_zero_sizes(gpu):
     e = torch.empty((0, 128), dtype=torch.uint8, device=gpu)
     w = torch.zeros((64, 128), dtype=torch.uint8, device=gpu)
     b = torch.zeros(1, dtype=torch.int32, device=gpu)
     y = F.fp8_linear_fwd(e, b, w, b)
     assert y.shape == (0, 64)
+    # an empty output has amax 0: the amax word is written, not left stale
+    am = torch.full((1,), 0x12345, dtype=torch.int32, device=gpu)
+    F.fp8_linear_fwd(e, b, w, b, y_amax_bits=am)
+    dxam = torch.full((1,), 0x12345, dtype=torch.int32, device=gpu)
+    F.fp8_linear_bwd_dx(e, b, torch.zeros((0, 128), dtype=torch.uint8, device=gpu), b, dx_amax_bits=dxam)
+    torch.cuda.synchronize()
+    assert u32(am) == 0 and u32(dxam) == 0
     # K == 0: zeros
     x0 = torch.empty((5, 0), dtype=torch.uint8, device=gpu)
     w0 = torch.empty((7, 0), dtype=torch.uint8, device=gpu)

@@ -67,8 +67,10 @@ def test_special_values_per_segment(orc, gpu):
     """A NaN in one segment, an all-zero segment, an infinity in another."""
     x = data(96, 40, 7, F.DT_BF16)
     x[5, 3] = float("nan")
+    x.view(torch.int16)[6, 8] = 0x7FC5      # a NaN with a payload: the amax is still 0x7FC00000
     x[40:64] = 0
     x[70, 1] = float("-inf")
+    x.view(torch.int16)[90, 2] = -93        # 0xFFA3: a negative NaN with a payload
     off = [0, 32, 40, 64, 96]
     q, qT, b, a, fl, rb = F.fp8_quantise_segments(x.to(gpu), torch.tensor(off, dtype=torch.int32, device=gpu),
                                                   F.E4M3, want_qT=True)
@@ -76,6 +78,8 @@ def test_special_values_per_segment(orc, gpu):
     oq, oqT, ob, oa, ofl, orb = orc.quantise_segments(np_bits(x), off, F.E4M3)
     assert b.cpu().tolist() == ob and (fl.cpu().numpy().view(np.uint32) == np.array(ofl, np.uint32)).all()
     assert ofl[0] == F.FLAG_NONFINITE and ofl[2] == F.FLAG_ZERO and ofl[3] == F.FLAG_NONFINITE
+    assert oa[0] == 0x7FC00000 and oa[3] == 0x7FC00000
+    assert (a.cpu().numpy().view(np.uint32) == np.array(oa, np.uint32)).all()
     assert np.array_equal(q.cpu().numpy(), oq) and np.array_equal(qT.cpu().numpy(), oqT)
 
 
