@@ -90,6 +90,9 @@ def parse(argv=None):
                    help="only run the register-operand FP8 MFMA loop of libfp8probe.so (ITERS x 8 "
                         "instructions per wave, 8 waves on each of 256 workgroups), --steps launches: the "
                         "sustained matrix-core rate with no memory traffic, then exit")
+    p.add_argument("--stream-ceiling", type=int, default=0, metavar="MB",
+                   help="only run the cast-shaped stream of libfp8probe.so on a bf16 tensor of MB megabytes "
+                        "(2 bytes read, 1 or 2 written per element), --steps launches each, then exit")
     p.add_argument("--no-configs", action="store_true",
                    help="time the chosen workload only (no table of the other workloads)")
     p.add_argument("--no-mispredicted", action="store_true",
@@ -530,39 +533,83 @@ def bench_workload(args, w, steps, warmup, cpu_baseline_budget=None, mispredicte
     return res
 
 
-def mfma_ceiling(args):
-    """Sustained FP8 matrix-core rate with no memory traffic (measurement aid
-    libfp8probe.so): HIP events around each launch on the current stream."""
+def probe_lib():
     import ctypes
-    import torch
     path = os.path.join(ROOT, "paper_2309_17224_amd", "libfp8probe.so")
     if not os.path.exists(path):
         raise SystemExit(f"{path} is missing: build it with `python -m paper_2309_17224_amd.build`")
     P = ctypes.CDLL(path)
     P.fp8probe_mfma_loop.restype = ctypes.c_int32
-    P.fp8probe_mfma_loop.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    P.fp8probe_mfma_loop.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                     ctypes.c_void_p]
     P.fp8probe_mfma_loop_flops.restype = ctypes.c_int64
     P.fp8probe_mfma_loop_flops.argtypes = [ctypes.c_int32, ctypes.c_int32]
+    P.fp8probe_stream.restype = ctypes.c_int32
+    P.fp8probe_stream.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                  ctypes.c_void_p]
+    return P
+
+
+def stream_ceiling(args):
+    """Read + write ceiling of a cast-shaped stream (measurement aid
+    libfp8probe.so): 2 bytes read and 1 (codes) or 2 (codes and a second
+    copy) written per element, HIP events around each launch."""
+    import ctypes
+    import torch
+    P = probe_lib()
+    n = (args.stream_ceiling << 20) // 2 // 8 * 8
+    src = torch.randn(n, dtype=torch.float32, device="cuda").to(torch.bfloat16)
+    d1 = torch.empty(n, dtype=torch.uint8, device="cuda")
+    d2 = torch.empty(n, dtype=torch.uint8, device="cuda")
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    res = {}
+    for label, second, nbytes in (("read2_write1", None, 3 * n), ("read2_write2", d2, 4 * n)):
+        ts = []
+        for i in range(max(args.warmup, 1) + args.steps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            st = P.fp8probe_stream(ctypes.c_void_p(src.data_ptr()), n, ctypes.c_void_p(d1.data_ptr()),
+                                   None if second is None else ctypes.c_void_p(second.data_ptr()), stream)
+            if st != 0:
+                raise SystemExit("fp8probe_stream failed")
+            b.record()
+            torch.cuda.synchronize()
+            if i >= max(args.warmup, 1):
+                ts.append(a.elapsed_time(b) * 1e-3)
+        med = sorted(ts)[len(ts) // 2]
+        res[label] = {"bytes_per_launch": nbytes, "median_us": med * 1e6, "GB_per_s": nbytes / med / 1e9,
+                      "frac_of_8TBps": nbytes / med / 8e12, "launches": len(ts)}
+    print(json.dumps({"stream": {"elements": n, "input_mb": 2 * n / 1e6, **res}}), flush=True)
+
+
+def mfma_ceiling(args):
+    """Sustained FP8 matrix-core rate with no memory traffic (measurement aid
+    libfp8probe.so): HIP events around each launch on the current stream."""
+    import ctypes
+    import torch
+    P = probe_lib()
     blocks, iters = torch.cuda.get_device_properties(0).multi_processor_count, args.mfma_ceiling
     out = torch.zeros(blocks * 8, dtype=torch.float32, device="cuda")
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
     flops = P.fp8probe_mfma_loop_flops(blocks, iters)
-    ts = []
-    for i in range(max(args.warmup, 1) + args.steps):
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        if P.fp8probe_mfma_loop(blocks, iters, ctypes.c_void_p(out.data_ptr()), stream) != 0:
-            raise SystemExit("fp8probe_mfma_loop failed")
-        b.record()
-        torch.cuda.synchronize()
-        if i >= max(args.warmup, 1):
-            ts.append(a.elapsed_time(b) * 1e-3)
-    med = sorted(ts)[len(ts) // 2]
+    res = {}
+    for vary in (1, 0):
+        ts = []
+        for i in range(max(args.warmup, 1) + args.steps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            if P.fp8probe_mfma_loop(blocks, iters, vary, ctypes.c_void_p(out.data_ptr()), stream) != 0:
+                raise SystemExit("fp8probe_mfma_loop failed")
+            b.record()
+            torch.cuda.synchronize()
+            if i >= max(args.warmup, 1):
+                ts.append(a.elapsed_time(b) * 1e-3)
+        med = sorted(ts)[len(ts) // 2]
+        res["random_operands" if vary else "fixed_operands"] = {
+            "median_s": med, "TFLOP_per_s": flops / med / 1e12,
+            "frac_of_fp8_peak": flops / med / 1e12 / FP8_PEAK_TFLOPS, "launches": len(ts)}
     print(json.dumps({"mfma_loop": {"workgroups": blocks, "waves_per_workgroup": 8, "iters": iters,
-                                    "flop_per_launch": flops, "median_s": med,
-                                    "TFLOP_per_s": flops / med / 1e12,
-                                    "frac_of_fp8_peak": flops / med / 1e12 / FP8_PEAK_TFLOPS,
-                                    "launches": len(ts)}}), flush=True)
+                                    "flop_per_launch": flops, **res}}), flush=True)
 
 
 def main(argv=None):
@@ -588,6 +635,9 @@ def main(argv=None):
         return
     if args.mfma_ceiling:
         mfma_ceiling(args)
+        return
+    if args.stream_ceiling:
+        stream_ceiling(args)
         return
     fp8lin.lib()  # fails loudly when the HIP library is missing
     if args.amax_mb:

@@ -82,6 +82,7 @@ extern "C" {
 /* Bits of *flags. */
 #define FP8_FLAG_NONFINITE 1u
 #define FP8_FLAG_ZERO 2u
+#define FP8_FLAG_SATURATED 4u  /* fp8_quantise_delayed: the codes of this call clipped */
 
 /* Largest accepted |margin|. */
 #define FP8_MAX_MARGIN 65536
@@ -187,6 +188,35 @@ int32_t fp8_quantise(const void *x, int32_t dt, int64_t rows, int64_t cols, int6
                      int32_t fmt, int32_t margin, const int32_t *bias_pred, int32_t *bias,
                      uint32_t *amax_bits, uint32_t *flags, uint8_t *q, int64_t ldq,
                      uint8_t *qT, int64_t ldqT, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * fp8_quantise_delayed -- delayed scaling: the remedy Sec. 3 cites for the
+ * second pass over a tensor that computing its bias just in time costs.  The
+ * bias comes from the amax of earlier calls, so the tensor is read once and
+ * its codes are never recast; a tensor that outgrows the bias clips (App. A).
+ *   codes  = cast(x * 2^(*bias))                (the bias on entry)
+ *   a      = amax(x)  (Eq. 3's amax of this tensor; NaN gives 0x7FC00000)
+ *   history[*count % history_len] = a;  *count += 1
+ *   *bias  = floor(log2(max_num / max(history))) - margin   (Eq. 3; the bias
+ *            of the next call; 0 when that maximum is zero or not finite)
+ * x, dt, rows, cols, ldx, fmt, q, ldq, qT, ldqT, ws, ws_bytes: as fp8_quantise.
+ * bias:        in/out, one int32 (device): the bias to cast with; replaced by
+ *              the next call's bias.
+ * history:     device uint32 [history_len], 1 <= history_len <= 65536: amax bit
+ *              patterns of earlier calls as this call writes them; zeros before
+ *              the first call.
+ * count:       device uint32: calls so far (the next slot is count % history_len).
+ * amax_bits:   out, optional: a.
+ * flags:       out, optional: FP8_FLAG_NONFINITE / FP8_FLAG_ZERO for a, else
+ *              FP8_FLAG_SATURATED when a * 2^bias > max_num (some codes clipped).
+ * rows == 0 or cols == 0: a = 0 is recorded, FP8_FLAG_ZERO, no codes.
+ * Calls that share a history must be ordered (one stream).
+ */
+int32_t fp8_quantise_delayed(const void *x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx,
+                             int32_t fmt, int32_t margin, int32_t *bias, uint32_t *history,
+                             int64_t history_len, uint32_t *count, uint32_t *amax_bits,
+                             uint32_t *flags, uint8_t *q, int64_t ldq, uint8_t *qT, int64_t ldqT,
+                             void *ws, size_t ws_bytes, void *stream);
 
 /*
  * fp8_quantise_batch -- fp8_quantise of n tensors (1 <= n <=

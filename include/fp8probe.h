@@ -5,10 +5,19 @@
  * fp8probe_mfma_loop -- launches `blocks` workgroups of 8 waves, each wave
  * issuing iters x 8 FP8 matrix instructions (v_mfma_f32_16x16x128_f8f6f4) on
  * register operands with no memory traffic, then writing one float per wave to
- * out (device, blocks * 8 floats, 4-byte aligned).  Asynchronous on stream.
+ * out (device, blocks * 8 floats, 4-byte aligned).  vary != 0: consecutive
+ * instructions take different pseudo-random operands (finite E4M3 codes), as
+ * in a matmul; vary == 0: every instruction the same operands.  Asynchronous
+ * on stream.
  * Returns 0, 1 for a bad argument (nothing launched) or 3 for a launch error.
  * fp8probe_mfma_loop_flops -- the FLOPs of one such launch (2 * 16 * 16 * 128
  * per instruction).
+ *
+ * fp8probe_stream -- the memory traffic of a cast with no arithmetic: reads n
+ * bf16 elements of src (device, 16-byte aligned, n a multiple of 8) and writes
+ * one byte per element to dst1 and, if dst2 is not NULL, one more to dst2
+ * (device, 8-byte aligned): 3 or 4 bytes per element, each workgroup a
+ * contiguous range, non-temporal loads and stores.  Returns as above.
  */
 #ifndef FP8PROBE_H
 #define FP8PROBE_H
@@ -20,7 +29,8 @@ extern "C" {
 #endif
 
 int64_t fp8probe_mfma_loop_flops(int32_t blocks, int32_t iters);
-int32_t fp8probe_mfma_loop(int32_t blocks, int32_t iters, float *out, void *stream);
+int32_t fp8probe_mfma_loop(int32_t blocks, int32_t iters, int32_t vary, float *out, void *stream);
+int32_t fp8probe_stream(const void *src, int64_t n, void *dst1, void *dst2, void *stream);
 
 #ifdef __cplusplus
 }

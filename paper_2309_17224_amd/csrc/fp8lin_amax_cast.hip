@@ -345,6 +345,49 @@ __global__ __launch_bounds__(kCastThreads) void quant_pass2_kernel(
                               vec_in, vec_q, vec_qT);
 }
 
+// ------------------------------------------------ delayed scaling
+// The second launch of fp8_quantise_delayed (one workgroup): the tensor's amax
+// from the tile maxima of pass 1 (cast with the bias in *bias, recorded in
+// *used), whether those codes clipped (amax * 2^used > max_num, i.e. used is
+// above the tensor's own Eq. 3 bias), the amax appended to the history ring
+// at *count % hlen, and the bias of the next call: Eq. 3 of the largest amax
+// in the history, minus the margin.  History words are amax bit patterns with
+// the sign clear (canonical NaN 0x7FC00000 largest), so their integer maximum
+// is the largest amax.  Slot *count % hlen is left out of the history
+// reduction and replaced by this tensor's amax, so no thread reads the word
+// thread 0 writes.
+template <int DT, int FMT>
+__global__ __launch_bounds__(kCastThreads) void quant_delayed_finish_kernel(
+    const uint32_t* __restrict__ parts, int nparts, const int32_t* __restrict__ used, int32_t margin,
+    uint32_t* __restrict__ history, int hlen, uint32_t* __restrict__ count, int32_t* __restrict__ bias,
+    uint32_t* __restrict__ amax_bits, uint32_t* __restrict__ flags) {
+    __shared__ uint32_t red[kCastThreads / 64];
+    __shared__ uint32_t slot_s;
+    uint32_t m = strided_max<kCastThreads>(parts, nparts);
+    m = block_max(m, red);
+    if (threadIdx.x == 0) slot_s = *count;
+    __syncthreads();
+    const uint32_t c = slot_s;
+    const int slot = (int)(c % (uint32_t)hlen);
+    uint32_t h = 0;
+    for (int i = threadIdx.x; i < hlen; i += kCastThreads)
+        if (i != slot) h = max(h, history[i]);
+    __syncthreads();  // red[] is reused
+    h = block_max(h, red);
+    if (threadIdx.x == 0) {
+        const uint32_t a32 = canon_amax(DT == FP8_DT_BF16 ? (m << 16) : m);
+        uint32_t fl;
+        const int32_t own = bias_of<FMT>(a32, 0, &fl);
+        if (fl == 0u && nparts > 0 && *used > own) fl = FP8_FLAG_SATURATED;
+        history[slot] = a32;
+        *count = c + 1u;
+        uint32_t fl_next;
+        *bias = bias_of<FMT>(max(h, a32), margin, &fl_next);
+        if (amax_bits) *amax_bits = a32;
+        if (flags) *flags = fl;
+    }
+}
+
 // ------------------------------------------------ quantise several tensors
 // fp8_quantise of up to kQBatch tensors of one element type and format in one
 // pass-1 launch and one pass-2 launch: workgroups [t0[i], t0[i+1]) of pass 1
@@ -504,6 +547,27 @@ void launch_quant_check_t(const void* x, int64_t rows, int64_t cols, int64_t ldx
     hipLaunchKernelGGL((quant_pass2_kernel<DT, FMT>), dim3(nb2), dim3(kCastThreads), 0, s, x, rows, cols, ldx,
                        parts, nparts, used, 1, margin, bias, amax_bits, flags, q, ldq, qT, ldqT, tiles_c, ncast,
                        vec_in, vec_q, vec_qT);
+}
+
+template <int DT, int FMT>
+void launch_quantise_delayed_t(const void* x, int64_t rows, int64_t cols, int64_t ldx, int32_t margin, int32_t* bias,
+                               uint32_t* history, int hlen, uint32_t* count, uint32_t* amax_bits, uint32_t* flags,
+                               uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT, uint32_t* ws, hipStream_t s) {
+    const int64_t tiles_r = (rows + kCastRows - 1) / kCastRows;
+    const int64_t tiles_c = (cols + kCastCols - 1) / kCastCols;
+    const int64_t ntiles = tiles_r * tiles_c;
+    int32_t* used = (int32_t*)ws;
+    uint32_t* parts = ws + 1;
+    if (ntiles > 0) {
+        const int esz = DT == FP8_DT_BF16 ? 2 : 4;
+        const int vec_in = ((uintptr_t)x % 16 == 0) && ((ldx * esz) % 16 == 0);
+        const int vec_q = q && ((uintptr_t)q % 8 == 0) && (ldq % 8 == 0);
+        const int vec_qT = qT && ((uintptr_t)qT % 16 == 0) && (ldqT % 16 == 0);
+        hipLaunchKernelGGL((quant_pass1_kernel<DT, FMT, true>), dim3((unsigned)ntiles), dim3(kCastThreads), 0, s, x,
+                           rows, cols, ldx, bias, used, parts, q, ldq, qT, ldqT, tiles_c, vec_in, vec_q, vec_qT);
+    }
+    hipLaunchKernelGGL((quant_delayed_finish_kernel<DT, FMT>), dim3(1), dim3(kCastThreads), 0, s, parts, (int)ntiles,
+                       used, margin, history, hlen, count, bias, amax_bits, flags);
 }
 
 // Host dispatch of (element type, format) to kernel template arguments.
@@ -740,6 +804,18 @@ int32_t launch_quant_check(const void* x, int dt, int64_t rows, int64_t cols, in
     with_dt_fmt(dt, fmt, [&](auto D, auto F) {
         launch_quant_check_t<decltype(D)::value, decltype(F)::value>(x, rows, cols, ldx, margin, parts, nparts, used,
                                                                      bias, amax_bits, flags, q, ldq, qT, ldqT, s);
+    });
+    return hip_status();
+}
+
+int32_t launch_quantise_delayed(const void* x, int dt, int64_t rows, int64_t cols, int64_t ldx, int fmt,
+                                int32_t margin, int32_t* bias, uint32_t* history, int hlen, uint32_t* count,
+                                uint32_t* amax_bits, uint32_t* flags, uint8_t* q, int64_t ldq, uint8_t* qT,
+                                int64_t ldqT, uint32_t* ws, hipStream_t s) {
+    with_dt_fmt(dt, fmt, [&](auto D, auto F) {
+        launch_quantise_delayed_t<decltype(D)::value, decltype(F)::value>(x, rows, cols, ldx, margin, bias, history,
+                                                                          hlen, count, amax_bits, flags, q, ldq, qT,
+                                                                          ldqT, ws, s);
     });
     return hip_status();
 }

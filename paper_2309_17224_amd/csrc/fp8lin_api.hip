@@ -177,6 +177,24 @@ int32_t fp8_quantise(const void* x, int32_t dt, int64_t rows, int64_t cols, int6
                            q, ldq, qT, ldqT, (uint32_t*)ws, as_stream(stream));
 }
 
+int32_t fp8_quantise_delayed(const void* x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx, int32_t fmt,
+                             int32_t margin, int32_t* bias, uint32_t* history, int64_t history_len, uint32_t* count,
+                             uint32_t* amax_bits, uint32_t* flags, uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT,
+                             void* ws, size_t ws_bytes, void* stream) {
+    bool empty;
+    const int32_t st = quantise_checks(x, dt, rows, cols, ldx, fmt, margin, nullptr, bias, amax_bits, flags, q, ldq,
+                                       qT, ldqT, &empty);
+    if (st != FP8_OK) return st;
+    if (history_len < 1 || history_len > 65536 || !history || !aligned(history, 4) || !count || !aligned(count, 4))
+        return FP8_EINVAL;
+    if (!ws || !aligned(ws, 4)) return FP8_EINVAL;
+    if (!empty && ws_bytes < fp8_quantise_ws_bytes(rows, cols)) return FP8_EINVAL;
+    if (empty && ws_bytes < sizeof(uint32_t)) return FP8_EINVAL;
+    return launch_quantise_delayed(x, dt, empty ? 0 : rows, empty ? 0 : cols, ldx, fmt, margin, bias, history,
+                                   (int)history_len, count, amax_bits, flags, q, ldq, qT, ldqT, (uint32_t*)ws,
+                                   as_stream(stream));
+}
+
 int32_t fp8_quantise_batch(int32_t n, const fp8_quantise_args* t, int32_t dt, int32_t fmt, int32_t margin,
                            void* stream) {
     if (n == 0) return FP8_OK;

@@ -53,6 +53,14 @@ int32_t launch_quantise(const void* x, int dt, int64_t rows, int64_t cols, int64
                         uint32_t* flags, uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT,
                         uint32_t* ws, hipStream_t s);
 
+// Delayed scaling: cast with *bias (one pass over x), then a one-workgroup
+// kernel appends the tensor's amax to history[*count % hlen], increments
+// *count and writes the next call's bias into *bias.  ws as launch_quantise.
+int32_t launch_quantise_delayed(const void* x, int dt, int64_t rows, int64_t cols, int64_t ldx, int fmt,
+                                int32_t margin, int32_t* bias, uint32_t* history, int hlen, uint32_t* count,
+                                uint32_t* amax_bits, uint32_t* flags, uint8_t* q, int64_t ldq, uint8_t* qT,
+                                int64_t ldqT, uint32_t* ws, hipStream_t s);
+
 // The exact-bias check and recast of fp8_quantise's second pass for a tensor
 // x whose per-tile maxima (nparts of them, any tiling) and the prediction its
 // codes were cast with (*used) were written by another kernel.

@@ -6,6 +6,11 @@
 // loop is not removed.  bench.py --mfma-ceiling launches it and reports
 // 2 * 16 * 16 * 128 FLOP per instruction over the launch time, the ceiling the
 // matmul kernels are compared with under the chip's sustained clock.
+// Operands: with `vary` the eight instructions of an iteration take four
+// different pseudo-random A and B fragments (every byte a finite E4M3 code),
+// so the multiplier inputs change from one instruction to the next as in a
+// matmul; without it every instruction reads the same fragments.  The power a
+// matrix core draws, and so the clock it sustains, depends on that.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -18,15 +23,32 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 
 constexpr int kAcc = 8;
 
-__global__ __launch_bounds__(512) void mfma_loop_kernel(int iters, uint32_t seed, float* __restrict__ out) {
-    // finite E4M3 codes of moderate size: bytes 0x30..0x3F (0.5 .. 0.94)
-    const uint32_t t = (seed + threadIdx.x * 2654435761u + blockIdx.x * 40503u) | 0x30303030u;
-    const uint32_t code = t & 0x3F3F3F3Fu;
-    v8i a, b;
+// xorshift32 step (a pseudo-random word per call)
+__device__ __forceinline__ uint32_t next_word(uint32_t& s) {
+    s ^= s << 13;
+    s ^= s >> 17;
+    s ^= s << 5;
+    return s;
+}
+
+__global__ __launch_bounds__(512) void mfma_loop_kernel(int iters, uint32_t seed, int vary, float* __restrict__ out) {
+    uint32_t st = seed ^ (threadIdx.x * 2654435761u) ^ (blockIdx.x * 40503u + 1u);
+    // random finite E4M3 codes: clearing bit 0x08 of each byte's exponent
+    // field keeps every byte below the NaN pattern S.1111.111
+    v8i a[4], b[4];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        a[i] = (int)(code ^ (uint32_t)(i * 0x01010101u & 0x07070707u));
-        b[i] = (int)(code ^ (uint32_t)((i + 3) * 0x01010101u & 0x07070707u));
+    for (int f = 0; f < 4; ++f)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            a[f][i] = (int)(next_word(st) & 0xF7F7F7F7u);
+            b[f][i] = (int)(next_word(st) & 0xF7F7F7F7u);
+        }
+    if (!vary) {
+#pragma unroll
+        for (int f = 1; f < 4; ++f) {
+            a[f] = a[0];
+            b[f] = b[0];
+        }
     }
     v4f acc[kAcc];
 #pragma unroll
@@ -34,7 +56,8 @@ __global__ __launch_bounds__(512) void mfma_loop_kernel(int iters, uint32_t seed
     for (int it = 0; it < iters; ++it) {
 #pragma unroll
         for (int j = 0; j < kAcc; ++j)
-            acc[j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, acc[j], 0, 0, 0, 0, 0, 0);
+            acc[j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a[j & 3], b[(j >> 1) & 3], acc[j], 0, 0, 0,
+                                                                      0, 0, 0);
     }
     float s = 0.f;
 #pragma unroll
@@ -42,17 +65,62 @@ __global__ __launch_bounds__(512) void mfma_loop_kernel(int iters, uint32_t seed
     if ((threadIdx.x & 63) == 0) out[blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)] = s;
 }
 
+// Cast-shaped stream: each workgroup reads one contiguous range of bf16
+// elements with eight 16-byte non-temporal loads in flight per lane and
+// writes one byte per element (the high byte of each bf16: no conversion
+// arithmetic) to dst1 and, if given, to dst2, with non-temporal stores.
+constexpr int kStreamThreads = 256, kStreamL = 8;
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+__global__ __launch_bounds__(kStreamThreads) void stream_kernel(const u32x4* __restrict__ src, int64_t nv,
+                                                                 u32x2* __restrict__ dst1, u32x2* __restrict__ dst2) {
+    const int64_t chunk = ((nv + gridDim.x - 1) / gridDim.x + 255) & ~(int64_t)255;
+    const int64_t b0 = min(nv, (int64_t)blockIdx.x * chunk), b1 = min(nv, b0 + chunk);
+    for (int64_t i = b0 + threadIdx.x; i < b1; i += kStreamL * kStreamThreads) {
+        u32x4 v[kStreamL];
+#pragma unroll
+        for (int l = 0; l < kStreamL; ++l) {
+            const int64_t j = min(i + l * kStreamThreads, b1 - 1);
+            v[l] = __builtin_nontemporal_load(src + j);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int l = 0; l < kStreamL; ++l) {
+            const int64_t j = i + l * kStreamThreads;
+            if (j < b1) {
+                const uint32_t lo = ((v[l].x >> 8) & 0xFFu) | ((v[l].x >> 16) & 0xFF00u) | ((v[l].y << 8) & 0xFF0000u) |
+                                    (v[l].y & 0xFF000000u);
+                const uint32_t hi = ((v[l].z >> 8) & 0xFFu) | ((v[l].z >> 16) & 0xFF00u) | ((v[l].w << 8) & 0xFF0000u) |
+                                    (v[l].w & 0xFF000000u);
+                __builtin_nontemporal_store(u32x2{lo, hi}, dst1 + j);
+                if (dst2) __builtin_nontemporal_store(u32x2{hi, lo}, dst2 + j);
+            }
+        }
+    }
+}
+
 }  // namespace
 
 extern "C" {
+
+int32_t fp8probe_stream(const void* src, int64_t n, void* dst1, void* dst2, void* stream) {
+    if (n < 8 || n % 8 || !src || !dst1 || ((uintptr_t)src % 16) || ((uintptr_t)dst1 % 8) ||
+        (dst2 && ((uintptr_t)dst2 % 8)))
+        return 1;
+    hipLaunchKernelGGL(stream_kernel, dim3(2048), dim3(kStreamThreads), 0, (hipStream_t)stream, (const u32x4*)src,
+                       n / 8, (u32x2*)dst1, (u32x2*)dst2);
+    return hipGetLastError() == hipSuccess ? 0 : 3;
+}
 
 int64_t fp8probe_mfma_loop_flops(int32_t blocks, int32_t iters) {
     return (int64_t)blocks * 8 * iters * kAcc * 2 * 16 * 16 * 128;
 }
 
-int32_t fp8probe_mfma_loop(int32_t blocks, int32_t iters, float* out, void* stream) {
+int32_t fp8probe_mfma_loop(int32_t blocks, int32_t iters, int32_t vary, float* out, void* stream) {
     if (blocks < 1 || blocks > 65536 || iters < 1 || !out || ((uintptr_t)out % 4)) return 1;
-    hipLaunchKernelGGL(mfma_loop_kernel, dim3(blocks), dim3(512), 0, (hipStream_t)stream, iters, 12345u, out);
+    hipLaunchKernelGGL(mfma_loop_kernel, dim3(blocks), dim3(512), 0, (hipStream_t)stream, iters, 12345u,
+                       vary ? 1 : 0, out);
     return hipGetLastError() == hipSuccess ? 0 : 3;
 }
 

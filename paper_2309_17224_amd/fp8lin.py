@@ -20,14 +20,14 @@ LIB_PATH = os.path.join(_HERE, "libfp8lin.so")
 E4M3, E5M2 = 0, 1
 E4_A, E5_A = 2, 3   # the paper's formats (Table 7 rows "(a)"); bias and cast calls only
 DT_BF16, DT_F32 = 0, 1
-FLAG_NONFINITE, FLAG_ZERO = 1, 2
+FLAG_NONFINITE, FLAG_ZERO, FLAG_SATURATED = 1, 2, 4
 OK, EINVAL, ENOTSUP, EHIP = 0, 1, 2, 3
 
 # Every symbol declared in include/fp8lin.h.
 EXPORTS = (
     "fp8_status_string", "fp8_abi_version", "fp8_scale_bias_ws_bytes", "fp8_scale_bias",
     "fp8_bias_from_amax", "fp8_cast_e4", "fp8_cast_e5", "fp8_cast", "fp8_quantise_ws_bytes",
-    "fp8_quantise",
+    "fp8_quantise", "fp8_quantise_delayed",
     "fp8_quantise_batch",
     "fp8_linear_fwd", "fp8_linear_bwd_dx", "fp8_linear_bias_ws_bytes", "fp8_linear_fwd_bias",
     "fp8_linear_bwd_dx_bias", "fp8_linear_quantise_ws_bytes",
@@ -78,6 +78,9 @@ def lib() -> ctypes.CDLL:
         L.fp8_quantise.restype = i32
         L.fp8_quantise.argtypes = [vp, i32, i64, i64, i64, i32, i32, vp, vp, vp, vp, vp, i64, vp,
                                    i64, vp, sz, vp]
+        L.fp8_quantise_delayed.restype = i32
+        L.fp8_quantise_delayed.argtypes = [vp, i32, i64, i64, i64, i32, i32, vp, vp, i64, vp, vp, vp, vp, i64,
+                                           vp, i64, vp, sz, vp]
         L.fp8_quantise_batch.argtypes = [i32, vp, i32, i32, i32, vp]
         L.fp8_quantise_batch.restype = i32
         for name in ("fp8_linear_fwd", "fp8_linear_bwd_dx"):
@@ -275,6 +278,31 @@ def fp8_quantise(x: torch.Tensor, fmt: int, margin: int = 0, bias_pred=None, bia
                             _ld(qT) if qT is not None else 0, _p(ws),
                             ws.numel() * ws.element_size(), _stream(stream))
     _check("fp8_quantise", st)
+    return q, qT, bias, amax_bits, flags
+
+
+def fp8_quantise_delayed(x: torch.Tensor, fmt: int, bias: torch.Tensor, history: torch.Tensor,
+                         count: torch.Tensor, margin: int = 0, amax_bits=None, flags=None, q=None, qT=None,
+                         want_q=True, want_qT=False, ws=None, stream=None):
+    """Delayed scaling: cast with *bias, append amax(x) to the history ring
+    and write the next call's bias (Eq. 3 of the history maximum) into bias.
+    history: int32 device tensor of history_len words (zeros at first);
+    count: one int32 device word.  Returns (q, qT, bias, amax_bits, flags)."""
+    x2 = x if x.dim() == 2 else x.reshape(1, -1)
+    rows, cols = x2.shape
+    dev = x.device
+    amax_bits = _i32(dev) if amax_bits is None else amax_bits
+    flags = _i32(dev) if flags is None else flags
+    if want_q and q is None:
+        q = torch.empty((rows, cols), dtype=torch.uint8, device=dev)
+    if want_qT and qT is None:
+        qT = torch.empty((cols, rows), dtype=torch.uint8, device=dev)
+    ws = quantise_workspace(rows, cols, dev) if ws is None else ws
+    st = lib().fp8_quantise_delayed(_p(x2), _dt(x2), rows, cols, _ld(x2), fmt, margin, _p(bias), _p(history),
+                                    history.numel(), _p(count), _p(amax_bits), _p(flags), _p(q),
+                                    _ld(q) if q is not None else 0, _p(qT), _ld(qT) if qT is not None else 0,
+                                    _p(ws), ws.numel() * ws.element_size(), _stream(stream))
+    _check("fp8_quantise_delayed", st)
     return q, qT, bias, amax_bits, flags
 
 

@@ -176,6 +176,11 @@ class WorkloadStep:
       "twopass":   fp8_quantise without a prediction (amax pass, then cast);
       "separate":  fp8_scale_bias followed by fp8_cast_e4/e5.
     All three give identical bits (FP8-AMAX, Sec. 2.3).
+      "delayed":   delayed scaling (the amax-history remedy of Sec. 3):
+                   fp8_quantise_delayed casts each tensor once with Eq. 3 of
+                   the largest amax of its last `history_len` steps (0 before
+                   the first), records its own amax, never recasts; a tensor
+                   that outgrows its history clips (App. A).
       "cscale":    FP8-CSCALE (Sec. 3): one constant bias `cscale_bias` for every
                    weight, activation and gradient; no amax, only the casts and
                    the matmuls (no epilogue amax either).
@@ -197,11 +202,11 @@ class WorkloadStep:
       on the Llama-2-70B MLP step (operand panels of two kernels share L2).
     """
 
-    QUANT_MODES = ("predicted", "twopass", "separate", "cscale")
+    QUANT_MODES = ("predicted", "twopass", "separate", "delayed", "cscale")
 
     def __init__(self, workload, tensors: dict, device, margin: int = 0, quant: str = "predicted",
                  cscale_bias: int = 0, fused_bias: bool = True, concurrent: bool = False,
-                 batch_quant: bool = True, share: "WorkloadStep | None" = None):
+                 batch_quant: bool = True, share: "WorkloadStep | None" = None, history_len: int = 16):
         """share: another step of the same workload whose FP8 buffers, biases
         and outputs this one uses (its own input tensors only): steps over two
         input sets that write one set of codes, each taking its bias
@@ -252,6 +257,14 @@ class WorkloadStep:
         # transposed-code bytes each quantise / cast call writes beyond its
         # algorithmic 3 bytes per element (layout overhead, reported apart)
         self.layout_bytes = {}
+        # delayed scaling: per tensor an amax history (zeros) and a call count
+        self.history_len = int(history_len)
+        self.hist = {}
+        if quant == "delayed":
+            for name in self.q:
+                self.hist[name] = (torch.zeros(self.history_len, dtype=torch.int32, device=device),
+                                   torch.zeros(1, dtype=torch.int32, device=device))
+                self.q[name].bias.zero_()
         self.concurrent = bool(concurrent) and self.dev.type == "cuda"
         self.batch_quant = bool(batch_quant) and not self.concurrent and quant in ("predicted", "twopass")
         self.side = torch.cuda.Stream(self.dev) if self.concurrent else None  # default priority
@@ -277,6 +290,13 @@ class WorkloadStep:
             return [(f"cast {name}", "cast", 3 * n,
                      lambda: cast(x, qt.bias, q=qt.q, qT=qt.qT, want_q=qt.q is not None,
                                   want_qT=qt.qT is not None))]
+        if self.quant == "delayed":
+            hist, count = self.hist[name]
+            self.layout_bytes[f"quantise {name}"] = self._layout(name)
+            return [(f"quantise {name}", "quantise", 3 * n,
+                     lambda: F.fp8_quantise_delayed(x, fmt, qt.bias, hist, count, margin, amax_bits=qt.amax,
+                                                    flags=qt.flags, q=qt.q, qT=qt.qT, want_q=qt.q is not None,
+                                                    want_qT=qt.qT is not None, ws=qt.qws))]
         if self.quant != "separate":
             pred = qt.bias if self.quant == "predicted" else None
             # one read of the tensor and its codes when the prediction holds

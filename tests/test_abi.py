@@ -246,6 +246,26 @@ def test_decoder_glue_rejects(L):
     assert L.llama_residual_add(NULL, NULL, NULL, 0, NULL) == F.OK
 
 
+def test_quantise_delayed_rejects(L):
+    f = L.fp8_quantise_delayed
+    # (x, dt, rows, cols, ldx, fmt, margin, bias, history, hlen, count, amax, flags, q, ldq, qT, ldqT, ws, ws_bytes, stream)
+    ok = (FAKE, 0, 4, 8, 8, 0, 0, FAKE, FAKE, 16, FAKE, NULL, NULL, FAKE, 8, NULL, 0, FAKE, 64, NULL)
+    def call(i, v):
+        a = list(ok)
+        a[i] = v
+        return f(*a)
+    assert call(5, 9) == F.EINVAL                 # format
+    assert call(7, NULL) == F.EINVAL              # bias
+    assert call(8, NULL) == F.EINVAL              # history
+    assert call(8, ODD) == F.EINVAL               # history alignment
+    assert call(9, 0) == F.EINVAL                 # history length
+    assert call(9, 65537) == F.EINVAL
+    assert call(10, NULL) == F.EINVAL             # count
+    assert call(17, NULL) == F.EINVAL             # workspace
+    assert call(18, 4) == F.EINVAL                # workspace too small
+    assert call(13, NULL) == F.EINVAL             # no output
+
+
 def test_quantise_batch_rejects(L):
     """fp8_quantise_batch checks every tensor as fp8_quantise does, plus the
     batch size and that predictions are given for all tensors or none."""
