@@ -190,6 +190,31 @@ int32_t fp8_quantise(const void *x, int32_t dt, int64_t rows, int64_t cols, int6
                      uint8_t *qT, int64_t ldqT, void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * fp8_quantise_noalloc -- fp8_quantise with no workspace argument, for callers
+ * that cannot allocate device memory: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation.  Same arguments as
+ * fp8_quantise without ws / ws_bytes, and the same outputs, bit for bit.
+ * Its scratch words sit in a static device array of FP8_NOALLOC_SCRATCH_BYTES
+ * bytes that each GPU the library runs on holds until the process ends; the
+ * call allocates and frees nothing.
+ * Limit: a tensor of at most FP8_NOALLOC_MAX_TILES tiles of 128 x 128
+ * elements, ceil(rows / 128) * ceil(cols / 128) (about 4.29e9 elements);
+ * FP8_EINVAL beyond.
+ * Sharing: every call on one GPU uses that GPU's one array.  Calls that may
+ * run at the same time on one GPU (other streams, other threads) race and give
+ * wrong results: order them on one stream.
+ * The stream must belong to the current device (FP8_EINVAL otherwise).  The
+ * first call on each device looks up the array's address there
+ * (hipGetSymbolAddress, no allocation); FP8_EHIP if that fails.
+ */
+#define FP8_NOALLOC_SCRATCH_BYTES 1048576
+#define FP8_NOALLOC_MAX_TILES 262143
+int32_t fp8_quantise_noalloc(const void *x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx,
+                             int32_t fmt, int32_t margin, const int32_t *bias_pred, int32_t *bias,
+                             uint32_t *amax_bits, uint32_t *flags, uint8_t *q, int64_t ldq,
+                             uint8_t *qT, int64_t ldqT, void *stream);
+
+/*
  * fp8_quantise_delayed -- delayed scaling: the remedy Sec. 3 cites for the
  * second pass over a tensor that computing its bias just in time costs.  The
  * bias comes from the amax of earlier calls, so the tensor is read once and

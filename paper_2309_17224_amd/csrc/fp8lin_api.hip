@@ -1,6 +1,8 @@
 // C entry points of libfp8lin.so (declared and documented in fp8lin.h).
 // Each call checks its arguments on the host, then enqueues kernels on the
 // caller's stream; nothing is allocated, kept or synchronised.
+#include <mutex>
+
 #include "fp8lin_internal.h"
 
 using namespace fp8lin;
@@ -175,6 +177,59 @@ int32_t fp8_quantise(const void* x, int32_t dt, int64_t rows, int64_t cols, int6
     if (!ws || !aligned(ws, 4) || ws_bytes < fp8_quantise_ws_bytes(rows, cols)) return FP8_EINVAL;
     return launch_quantise(x, dt, rows, cols, ldx, fmt, margin, bias_pred, bias, amax_bits, flags,
                            q, ldq, qT, ldqT, (uint32_t*)ws, as_stream(stream));
+}
+
+}  // extern "C"
+
+// ---- fp8_quantise without a caller workspace (fp8_quantise_noalloc)
+// The quantise's scratch words (the prediction the codes were cast with, one
+// maximum per 128 x 128 tile) live in this file-scope device array; every GPU
+// the library runs on holds its own copy until the process ends.  Host code
+// never uses the array's name as an address: each device's address comes
+// from hipGetSymbolAddress, taken once with that device current.
+static __device__ __align__(256) uint32_t scratch[FP8_NOALLOC_SCRATCH_BYTES / sizeof(uint32_t)];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+uint32_t* g_scratch_ptr[kMaxDevices];  // per device; null until resolved
+
+// Device address of the current device's scratch array.
+int32_t current_scratch(uint32_t** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return FP8_EHIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return FP8_EHIP;
+        g_scratch_ptr[dev] = (uint32_t*)p;
+    }
+    *out = g_scratch_ptr[dev];
+    return FP8_OK;
+}
+}  // namespace
+
+extern "C" {
+
+int32_t fp8_quantise_noalloc(const void* x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx, int32_t fmt,
+                             int32_t margin, const int32_t* bias_pred, int32_t* bias, uint32_t* amax_bits,
+                             uint32_t* flags, uint8_t* q, int64_t ldq, uint8_t* qT, int64_t ldqT, void* stream) {
+    bool empty;
+    const int32_t st = quantise_checks(x, dt, rows, cols, ldx, fmt, margin, bias_pred, bias, amax_bits, flags, q,
+                                       ldq, qT, ldqT, &empty);
+    if (st != FP8_OK) return st;
+    if (empty) return launch_scale_bias(x, dt, 0, fmt, margin, bias, amax_bits, flags, nullptr, as_stream(stream));
+    if (quantise_tiles_upto(rows, cols, FP8_NOALLOC_MAX_TILES) < 0) return FP8_EINVAL;
+    int cur = -1;
+    hipDevice_t sdev = -1;
+    if (hipGetDevice(&cur) != hipSuccess || hipStreamGetDevice(as_stream(stream), &sdev) != hipSuccess)
+        return FP8_EHIP;
+    if (sdev != cur) return FP8_EINVAL;  // the scratch address is the current device's
+    uint32_t* ws = nullptr;
+    const int32_t sst = current_scratch(&ws);
+    if (sst != FP8_OK) return sst;
+    return launch_quantise(x, dt, rows, cols, ldx, fmt, margin, bias_pred, bias, amax_bits, flags, q, ldq, qT, ldqT,
+                           ws, as_stream(stream));
 }
 
 int32_t fp8_quantise_delayed(const void* x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx, int32_t fmt,

@@ -27,7 +27,7 @@ OK, EINVAL, ENOTSUP, EHIP = 0, 1, 2, 3
 EXPORTS = (
     "fp8_status_string", "fp8_abi_version", "fp8_scale_bias_ws_bytes", "fp8_scale_bias",
     "fp8_bias_from_amax", "fp8_cast_e4", "fp8_cast_e5", "fp8_cast", "fp8_quantise_ws_bytes",
-    "fp8_quantise", "fp8_quantise_delayed",
+    "fp8_quantise", "fp8_quantise_noalloc", "fp8_quantise_delayed",
     "fp8_quantise_batch",
     "fp8_linear_fwd", "fp8_linear_bwd_dx", "fp8_linear_bias_ws_bytes", "fp8_linear_fwd_bias",
     "fp8_linear_bwd_dx_bias", "fp8_linear_quantise_ws_bytes",
@@ -78,6 +78,9 @@ def lib() -> ctypes.CDLL:
         L.fp8_quantise.restype = i32
         L.fp8_quantise.argtypes = [vp, i32, i64, i64, i64, i32, i32, vp, vp, vp, vp, vp, i64, vp,
                                    i64, vp, sz, vp]
+        L.fp8_quantise_noalloc.restype = i32
+        L.fp8_quantise_noalloc.argtypes = [vp, i32, i64, i64, i64, i32, i32, vp, vp, vp, vp, vp, i64, vp,
+                                           i64, vp]
         L.fp8_quantise_delayed.restype = i32
         L.fp8_quantise_delayed.argtypes = [vp, i32, i64, i64, i64, i32, i32, vp, vp, i64, vp, vp, vp, vp, i64,
                                            vp, i64, vp, sz, vp]
@@ -303,6 +306,34 @@ def fp8_quantise_delayed(x: torch.Tensor, fmt: int, bias: torch.Tensor, history:
                                     _ld(q) if q is not None else 0, _p(qT), _ld(qT) if qT is not None else 0,
                                     _p(ws), ws.numel() * ws.element_size(), _stream(stream))
     _check("fp8_quantise_delayed", st)
+    return q, qT, bias, amax_bits, flags
+
+
+NOALLOC_SCRATCH_BYTES = 1048576
+NOALLOC_MAX_TILES = 262143
+
+
+def fp8_quantise_noalloc(x: torch.Tensor, fmt: int, margin: int = 0, bias_pred=None, bias=None,
+                         amax_bits=None, flags=None, q=None, qT=None, want_q=True, want_qT=False,
+                         stream=None):
+    """fp8_quantise with the library's static scratch instead of a workspace
+    (nothing allocated by the library; outputs are allocated here only when
+    not given).  Returns (q, qT, bias, amax_bits, flags)."""
+    x2 = x if x.dim() == 2 else x.reshape(1, -1)
+    rows, cols = x2.shape
+    dev = x.device
+    bias = _i32(dev) if bias is None else bias
+    amax_bits = _i32(dev) if amax_bits is None else amax_bits
+    flags = _i32(dev) if flags is None else flags
+    if want_q and q is None:
+        q = torch.empty((rows, cols), dtype=torch.uint8, device=dev)
+    if want_qT and qT is None:
+        qT = torch.empty((cols, rows), dtype=torch.uint8, device=dev)
+    st = lib().fp8_quantise_noalloc(_p(x2), _dt(x2), rows, cols, _ld(x2), fmt, margin, _p(bias_pred),
+                                    _p(bias), _p(amax_bits), _p(flags), _p(q),
+                                    _ld(q) if q is not None else 0, _p(qT),
+                                    _ld(qT) if qT is not None else 0, _stream(stream))
+    _check("fp8_quantise_noalloc", st)
     return q, qT, bias, amax_bits, flags
 
 

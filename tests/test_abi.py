@@ -246,6 +246,19 @@ def test_decoder_glue_rejects(L):
     assert L.llama_residual_add(NULL, NULL, NULL, 0, NULL) == F.OK
 
 
+def test_quantise_noalloc_rejects(L):
+    f = L.fp8_quantise_noalloc
+    # (x, dt, rows, cols, ldx, fmt, margin, pred, bias, amax, flags, q, ldq, qT, ldqT, stream)
+    assert f(FAKE, 0, 4, 8, 8, 9, 0, NULL, FAKE, NULL, NULL, FAKE, 8, NULL, 0, NULL) == F.EINVAL     # format
+    assert f(FAKE, 0, 4, 8, 8, 0, 0, NULL, NULL, NULL, NULL, FAKE, 8, NULL, 0, NULL) == F.EINVAL     # bias
+    assert f(FAKE, 0, 4, 8, 8, 0, 0, NULL, FAKE, NULL, NULL, NULL, 8, NULL, 0, NULL) == F.EINVAL     # no output
+    assert f(FAKE, 0, 4, 8, 4, 0, 0, NULL, FAKE, NULL, NULL, FAKE, 8, NULL, 0, NULL) == F.EINVAL     # ldx
+    # more 128 x 128 tiles than the static scratch holds (512 x 513 > 262143)
+    r, c = 512 * 128, 513 * 128
+    assert f(FAKE, 0, r, c, c, 0, 0, NULL, FAKE, NULL, NULL, FAKE, c, NULL, 0, NULL) == F.EINVAL
+    assert F.NOALLOC_SCRATCH_BYTES == 4 * (F.NOALLOC_MAX_TILES + 1)
+
+
 def test_quantise_delayed_rejects(L):
     f = L.fp8_quantise_delayed
     # (x, dt, rows, cols, ldx, fmt, margin, bias, history, hlen, count, amax, flags, q, ldq, qT, ldqT, ws, ws_bytes, stream)
