@@ -454,6 +454,36 @@ def quantise_table(step, per_call):
     return out
 
 
+def stream_ceilings(mb=1024, launches=5):
+    """Measured read + write ceilings of a cast-shaped stream (libfp8probe.so):
+    GB/s for 2 bytes read + 1 written and 2 read + 2 written per element."""
+    import ctypes
+    import torch
+    P = probe_lib()
+    n = (mb << 20) // 2 // 8 * 8
+    src = torch.zeros(n, dtype=torch.bfloat16, device="cuda")
+    d1 = torch.empty(n, dtype=torch.uint8, device="cuda")
+    d2 = torch.empty(n, dtype=torch.uint8, device="cuda")
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    out = {}
+    for label, second, nbytes in (("read2_write1", None, 3 * n), ("read2_write2", d2, 4 * n)):
+        ts = []
+        for i in range(launches + 2):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            if P.fp8probe_stream(ctypes.c_void_p(src.data_ptr()), n, ctypes.c_void_p(d1.data_ptr()),
+                                 None if second is None else ctypes.c_void_p(second.data_ptr()), stream) != 0:
+                raise SystemExit("fp8probe_stream failed")
+            b.record()
+            torch.cuda.synchronize()
+            if i >= 2:
+                ts.append(a.elapsed_time(b) * 1e-3)
+        out[label] = round(nbytes / sorted(ts)[len(ts) // 2] / 1e9, 1)
+    del src, d1, d2
+    torch.cuda.empty_cache()
+    return out
+
+
 def input_hashes(cpu):
     from paper_2309_17224_amd import workloads as wl
     h = {k: wl.sha256(v) for k, v in cpu.items()}
@@ -664,6 +694,8 @@ def main(argv=None):
         bench_layer(args, wl.LAYERS[args.workload])
         return
     w = wl.WORKLOADS[args.workload]
+    ceil = stream_ceilings()
+    log(f"[bench] cast-shaped stream ceilings (GB/s): {ceil}")
     res = bench_workload(args, w, args.steps, args.warmup,
                          cpu_baseline_budget=None if args.no_cpu_baseline else args.cpu_budget,
                          mispredicted=not args.no_mispredicted)
@@ -673,6 +705,13 @@ def main(argv=None):
            "vs_baseline": None, "dtype": "fp8", "data": "synthetic", "config": res.pop("config")}
     out.update(res)
     out.setdefault("cpu_baseline", None)
+    # every quantise call against HBM peak (3 bytes per element) and against the
+    # measured ceiling of a stream with the same bytes read and written
+    out["quantise_ceiling_GBps"] = {**ceil, "source": "libfp8probe.so stream, 1 GiB bf16, HIP events"}
+    for q in out.get("quantise_calls", []):
+        wr2 = q["transpose_bytes"] > 0
+        c = ceil["read2_write2"] if wr2 else ceil["read2_write1"]
+        q["frac_of_ceiling"] = round(q["GB_per_s_incl_transpose" if wr2 else "GB_per_s"] / c, 4)
     if not args.no_configs and args.workload == DEFAULT_WORKLOAD:
         side = {}
         for name in SIDE_WORKLOADS:

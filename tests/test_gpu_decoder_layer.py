@@ -117,6 +117,24 @@ def test_layer_7b_shape_matches_oracle(gpu):
     compare(cfg, layer, p, r)
 
 
+@pytest.mark.timeout(900)
+def test_70b_layer_full_size_matches_oracle(gpu):
+    """The Llama 2 70B layer at 2048 tokens, the configuration the benchmark
+    times, against the oracle chain computing every stage itself in fp64
+    (each activation's Eq. 3 bias needs the whole tensor, so the oracle runs
+    the whole chain: about two minutes of host time).  Same bars as the
+    smaller layers."""
+    cfg = wl.LAYERS["llama2-70b-layer"]
+    T = layer_inputs(cfg)
+    layer = gpu_layer(cfg, T, gpu)
+    layer.run()
+    layer.run()
+    torch.cuda.synchronize()
+    p, r = oracle_layer(cfg, T)
+    errs = compare(cfg, layer, p, r)
+    print("70B layer rel_F per stage:", {k: f"{v:.3e}" for k, v in errs.items()}, flush=True)
+
+
 def test_70b_layer_full_size_properties(gpu):
     """Llama 2 70B layer at 2048 tokens, the configuration the benchmark
     times: properties that hold at any size (the oracle chain at this size
