@@ -164,10 +164,13 @@ def time_steps(step, steps, warmup, flush=None):
     return wall, per_call, flush_s
 
 
-def time_graph(step, steps, warmup, flush=None):
-    """Wall time of `steps` replays of the captured step (HIP graph)."""
+def time_graph(step, steps, warmup, flush=None, capture=True):
+    """Wall time of `steps` replays of the captured step (HIP graph).  With
+    capture=False the step was captured beforehand (so that no idle gap for
+    the capture lets the clocks fall right before the timed replays)."""
     import torch
-    step.capture()
+    if capture:
+        step.capture()
     for _ in range(warmup):
         if flush is not None:
             flush.add_(1)
@@ -422,7 +425,7 @@ def time_alternating(step_a, step_b, steps, warmup):
     import torch
     step_a.capture()
     step_b.capture()
-    for _ in range(max(warmup, 1)):
+    for _ in range(max(warmup, 5)):
         step_a.replay()
         step_b.replay()
     torch.cuda.synchronize()
@@ -509,12 +512,18 @@ def bench_workload(args, w, steps, warmup, cpu_baseline_budget=None, mispredicte
     if args.flush_mb:
         flush = torch.zeros(args.flush_mb * (1 << 20) // 4, dtype=torch.float32, device=dev)
     log(f"[bench] {w.name}: {len(step.calls)} calls per step; warmup {warmup}, steps {steps}")
+    if args.launch == "graph":
+        # one untimed eager step, then the capture, both before any timing: the
+        # GPU then stays busy from the eager pass into the replays (an idle gap
+        # lets the clocks drop and the first timed replays run slow)
+        step.run()
+        step.capture()
     # eager pass: every call bracketed by HIP events on its stream (roofline table)
     wall, per_call, flush_s = time_steps(step, steps, warmup, flush)
     eager_step_s = (wall - flush_s) / steps
     step_s = eager_step_s
     if args.launch == "graph":
-        gwall, gflush = time_graph(step, steps, warmup, flush)
+        gwall, gflush = time_graph(step, steps, warmup, flush, capture=False)
         step_s = (gwall - gflush) / steps
     hits = step.prediction_hits()
     flops = step.gemm_flops()

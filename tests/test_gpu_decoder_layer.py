@@ -137,9 +137,8 @@ def test_70b_layer_full_size_matches_oracle(gpu):
 
 def test_70b_layer_full_size_properties(gpu):
     """Llama 2 70B layer at 2048 tokens, the configuration the benchmark
-    times: properties that hold at any size (the oracle chain at this size
-    needs minutes of CPU time; the kernels are compared with the oracle at
-    these shapes in test_gpu_decoder.py).  Inputs are drawn on the GPU."""
+    times: properties that hold at any size, on inputs drawn on the GPU (the
+    comparison with the oracle chain at this size is the test above)."""
     from paper_2309_17224_amd import fp8lin as F
     cfg = wl.LAYERS["llama2-70b-layer"]
     g = torch.Generator(device=gpu)
