@@ -337,8 +337,11 @@ int32_t fp8_bias_mode(const int32_t *bias, int64_t n, int32_t *ring, int64_t cap
  * its element size; FP8_EINVAL otherwise.
  * Kernels: K a multiple of 128 runs the matrix-core kernels that stage whole
  * 128-byte rows of both operands through LDS; any other K runs a 64 x 64 tile
- * kernel that loads single bytes with bounds checks: the same results, about
- * 3x the time of the staged kernels on large shapes.
+ * kernel with bounds checks and zero fill, the same results: with K a
+ * multiple of 16 it loads 16-byte chunks and takes about 4x the time of the
+ * staged kernels (measured 4096 x 4096 x 4032: 225 us against 63 us for
+ * K = 4096; 4096 x 11008 x 4032: 640 us against 147 us); with any other K
+ * it loads single bytes, about 40x.
  * The same rules hold for every matmul entry point below.
  */
 int32_t fp8_linear_fwd(const uint8_t *x8, const int32_t *bx, const uint8_t *w8t, const int32_t *bw,

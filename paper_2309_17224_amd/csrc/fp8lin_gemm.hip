@@ -40,7 +40,8 @@
 //    groups of 8 tile-rows, so tiles sharing operand panels meet in the same
 //    L2.
 // Decode kernel (M <= 32): weight-streaming split-K, see below.
-// Fallback kernel (any K or alignment): 64 x 64 tiles, byte loads with
+// Fallback kernel (K not a multiple of 128, or K >= 2^22): 64 x 64 tiles,
+// 16-byte loads when K is a multiple of 16 and byte loads otherwise, with
 // bounds checks and zero fill, same MFMA and epilogue.
 #include "fp8lin_fp8.h"
 #include "fp8lin_internal.h"
@@ -626,6 +627,10 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_small(
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
+    // K a multiple of 16 with 16-byte aligned operands: every row starts on a
+    // 16-byte boundary and each 16-byte chunk lies wholly inside or wholly
+    // past the row, so chunks are loaded whole (zero past the row end).
+    const bool v16 = (K & 15) == 0 && (((uintptr_t)A | (uintptr_t)B) & 15) == 0;
     for (int64_t k0 = 0; k0 < K; k0 += kBK) {
 #pragma unroll
         for (int op = 0; op < 2; ++op) {
@@ -636,14 +641,21 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_small(
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const int c = 2 * lq + h;  // logical 16-byte chunk
-                uint32_t wv[4] = {0, 0, 0, 0};
-                for (int t = 0; t < 16; ++t) {
-                    const int64_t k = k0 + c * 16 + t;
-                    uint32_t byte = 0;
-                    if (r < rmax && k < K) byte = src[r * K + k];
-                    wv[t >> 2] |= byte << (8 * (t & 3));
+                uint4 v = make_uint4(0, 0, 0, 0);
+                if (v16) {
+                    const int64_t k = k0 + c * 16;
+                    if (r < rmax && k < K) v = *(const uint4*)(src + r * K + k);
+                } else {
+                    uint32_t wv[4] = {0, 0, 0, 0};
+                    for (int t = 0; t < 16; ++t) {
+                        const int64_t k = k0 + c * 16 + t;
+                        uint32_t byte = 0;
+                        if (r < rmax && k < K) byte = src[r * K + k];
+                        wv[t >> 2] |= byte << (8 * (t & 3));
+                    }
+                    v = make_uint4(wv[0], wv[1], wv[2], wv[3]);
                 }
-                *(uint4*)(dst + lr * kBK + ((c ^ chunk_swz(lr)) << 4)) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+                *(uint4*)(dst + lr * kBK + ((c ^ chunk_swz(lr)) << 4)) = v;
             }
         }
         __syncthreads();

@@ -43,7 +43,8 @@ def run_nt(entry, A, fa, ba, B, fb, bb, out_dt, gpu, M, N, K, amax=False):
 
 ENTRY_FMTS = {"fwd": (0, 0), "dx": (1, 0), "dw": (0, 1)}
 SHAPES = [(1, 1, 128), (16, 16, 128), (256, 256, 256), (300, 200, 384), (17, 129, 1000),
-          (255, 1, 17), (1, 255, 640), (129, 257, 128), (513, 300, 512), (64, 64, 0), (5, 70, 1024)]
+          (255, 1, 17), (1, 255, 640), (129, 257, 128), (513, 300, 512), (64, 64, 0), (5, 70, 1024),
+          (300, 200, 400), (65, 257, 144), (40, 33, 16)]
 
 
 def scaled_normal_codes(shape, fmt, rng, orc):
