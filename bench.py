@@ -90,6 +90,8 @@ def parse(argv=None):
                    help="only run the register-operand FP8 MFMA loop of libfp8probe.so (ITERS x 8 "
                         "instructions per wave, 8 waves on each of 256 workgroups), --steps launches: the "
                         "sustained matrix-core rate with no memory traffic, then exit")
+    p.add_argument("--lds-probe", type=int, default=0, metavar="ITERS",
+                   help="time the LDS read / LDS-copy probe of libfp8probe.so (ITERS loop trips) and exit")
     p.add_argument("--stream-ceiling", type=int, default=0, metavar="MB",
                    help="only run the cast-shaped stream of libfp8probe.so on a bf16 tensor of MB megabytes "
                         "(2 bytes read, 1 or 2 written per element), --steps launches each, then exit")
@@ -529,6 +531,16 @@ def bench_workload(args, w, steps, warmup, cpu_baseline_budget=None, mispredicte
     flops = step.gemm_flops()
     roof, table = roofline(step, per_call)
     roof["traffic"] = measured_traffic(w.name, roof["kernel"])
+    # The whole step at the rooflines (each call's work at the MFMA or HBM
+    # peak): a step that takes far longer than that is bound by launch and
+    # ramp latency, and no roofline fraction is claimed for it.
+    floor_s = sum(work / (FP8_PEAK_TFLOPS * 1e12) if kind.startswith("gemm") and kind != "gemm_decode"
+                  else work / (HBM_PEAK_GBS * 1e9) for _, kind, work, _ in step.calls)
+    if floor_s < 0.1 * step_s:
+        roof = {"bound": "latency", "achieved": None, "peak": None, "unit": None, "frac": None, "traffic": None,
+                "kernel": roof["kernel"], "avg_launch_us": roof["avg_launch_us"],
+                "note": "step at the rooflines %.1f us against %.1f us measured: launch-latency bound, "
+                        "no roofline fraction claimed" % (floor_s * 1e6, step_s * 1e6)}
     for kind, d in sorted(table.items()):
         log(f"[bench] {kind:11s} " + " ".join(f"{k}={v:.4g}" if isinstance(v, float) else f"{k}={v}"
                                                for k, v in d.items()))
@@ -586,7 +598,47 @@ def probe_lib():
     P.fp8probe_stream.restype = ctypes.c_int32
     P.fp8probe_stream.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
                                   ctypes.c_void_p]
+    P.fp8probe_lds_src_bytes.restype = ctypes.c_int64
+    P.fp8probe_lds_src_bytes.argtypes = []
+    P.fp8probe_lds.restype = ctypes.c_int32
+    P.fp8probe_lds.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     return P
+
+
+def lds_probe(args):
+    """LDS read and LDS-copy rates per compute unit of the matmul's main-loop
+    traffic in isolation (measurement aid libfp8probe.so): 256 workgroups of
+    8 waves, HIP events around each launch; bytes per compute unit = waves x
+    iters x 8 KiB for each role."""
+    import ctypes
+    import torch
+    P = probe_lib()
+    src = torch.ones(int(P.fp8probe_lds_src_bytes()), dtype=torch.uint8, device="cuda")
+    out = torch.zeros(256, dtype=torch.int32, device="cuda")
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    iters = args.lds_probe
+    roles = {0: (8, 0), 1: (0, 8), 2: (4, 4), 3: (4, 0)}  # (reading waves, copying waves)
+    names = {0: "read_8_waves", 1: "copy_8_waves", 2: "copy_4_read_4", 3: "read_4_waves"}
+    res = {}
+    for mode in (0, 1, 2, 3):
+        ts = []
+        for i in range(max(args.warmup, 1) + args.steps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            if P.fp8probe_lds(mode, iters, ctypes.c_void_p(src.data_ptr()), ctypes.c_void_p(out.data_ptr()),
+                              stream) != 0:
+                raise SystemExit("fp8probe_lds failed")
+            b.record()
+            torch.cuda.synchronize()
+            if i >= max(args.warmup, 1):
+                ts.append(a.elapsed_time(b) * 1e-3)
+        med = sorted(ts)[len(ts) // 2]
+        rd, cp = roles[mode]
+        per = iters * 8 * 1024
+        res[names[mode]] = {"median_us": round(med * 1e6, 1),
+                            "read_GB_per_s_per_cu": round(rd * per / med / 1e9, 1),
+                            "copy_GB_per_s_per_cu": round(cp * per / med / 1e9, 1), "launches": len(ts)}
+    print(json.dumps({"lds_probe": {"workgroups": 256, "iters": iters, **res}}), flush=True)
 
 
 def stream_ceiling(args):
@@ -677,6 +729,9 @@ def main(argv=None):
         return
     if args.stream_ceiling:
         stream_ceiling(args)
+        return
+    if args.lds_probe:
+        lds_probe(args)
         return
     fp8lin.lib()  # fails loudly when the HIP library is missing
     if args.amax_mb:

@@ -18,6 +18,14 @@
  * one byte per element to dst1 and, if dst2 is not NULL, one more to dst2
  * (device, 8-byte aligned): 3 or 4 bytes per element, each workgroup a
  * contiguous range, non-temporal loads and stores.  Returns as above.
+ *
+ * fp8probe_lds -- LDS traffic of the matmul's main loop in isolation: 256
+ * workgroups of 8 waves, each wave iters x 8 ds_read_b128 of 1 KiB and/or
+ * iters x 8 global_load_lds_dwordx4 copies of 1 KiB into its own 8 KiB of LDS
+ * (mode 0: 8 waves read; 1: 8 waves copy; 2: 4 copy while 4 read; 3: 4 read).
+ * src: device, 16-byte aligned, fp8probe_lds_src_bytes() readable bytes (each
+ * workgroup copies from its own 1 MiB window); out: device, 256 uint32,
+ * written only by a practically impossible data pattern.  Returns as above.
  */
 #ifndef FP8PROBE_H
 #define FP8PROBE_H
@@ -31,6 +39,8 @@ extern "C" {
 int64_t fp8probe_mfma_loop_flops(int32_t blocks, int32_t iters);
 int32_t fp8probe_mfma_loop(int32_t blocks, int32_t iters, int32_t vary, float *out, void *stream);
 int32_t fp8probe_stream(const void *src, int64_t n, void *dst1, void *dst2, void *stream);
+int64_t fp8probe_lds_src_bytes(void);
+int32_t fp8probe_lds(int32_t mode, int32_t iters, const void *src, uint32_t *out, void *stream);
 
 #ifdef __cplusplus
 }

@@ -100,9 +100,69 @@ __global__ __launch_bounds__(kStreamThreads) void stream_kernel(const u32x4* __r
     }
 }
 
+// LDS traffic of the matmul's main loop in isolation: one workgroup of 8
+// waves per compute unit, each wave owning an 8 KiB region of LDS laid out as
+// eight 1 KiB rows of 16-byte chunks.  Readers issue ds_read_b128 over their
+// region (every lane a different chunk, every bank once per phase); copiers
+// fill their region from global memory with global_load_lds_dwordx4 (1 KiB
+// per instruction, up to 16 in flight per wave), reading a 1 MiB window of src
+// per workgroup so that the data comes from L2.  mode 0: all 8 waves read;
+// 1: all 8 copy; 2: waves 0-3 copy while 4-7 read; 3: waves 0-3 read, 4-7 idle.
+constexpr int kLdsRegion = 8192, kLdsWindow = 1 << 20;
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
+}
+
+__global__ __launch_bounds__(512) void lds_probe_kernel(int mode, int iters, const uint8_t* __restrict__ src,
+                                                        uint32_t* __restrict__ out) {
+    // 128 KiB (half unused) so that one workgroup fills a compute unit's LDS
+    // and every compute unit runs exactly one
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[16 * kLdsRegion];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    for (int i = threadIdx.x; i < 8 * kLdsRegion / 4; i += 512) ((uint32_t*)smem)[i] = (uint32_t)i;
+    __syncthreads();
+    const bool copy = mode == 1 || (mode == 2 && w < 4);
+    const bool read = mode == 0 || (mode == 2 && w >= 4) || (mode == 3 && w < 4);
+    const uint8_t* region = smem + w * kLdsRegion;
+    const uint8_t* window = src + (size_t)(blockIdx.x % 64) * kLdsWindow;
+    const uint32_t dst = __builtin_amdgcn_readfirstlane(lds_addr(region));
+    u32x4 x = {0u, 0u, 0u, 0u};
+    for (int it = 0; it < iters; ++it) {
+        if (read) {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) x ^= *(const u32x4*)(region + q * 1024 + lane * 16);
+        }
+        if (copy) {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const uint32_t off = (uint32_t)((((it * 8 + q) & (kLdsWindow / 1024 - 1)) * 1024) + lane * 16);
+                asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+                             :
+                             : "s"(dst + q * 1024), "v"(off), "s"(window)
+                             : "memory");
+            }
+            asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+        }
+        asm volatile("" ::: "memory");
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    if (x.x == 0x9E3779B9u) out[blockIdx.x] = x.y;  // keeps the reads; practically never taken
+}
+
 }  // namespace
 
 extern "C" {
+
+int64_t fp8probe_lds_src_bytes(void) { return (int64_t)64 * kLdsWindow; }
+
+int32_t fp8probe_lds(int32_t mode, int32_t iters, const void* src, uint32_t* out, void* stream) {
+    if (mode < 0 || mode > 3 || iters < 1 || !src || !out || ((uintptr_t)src % 16) || ((uintptr_t)out % 4))
+        return 1;
+    hipLaunchKernelGGL(lds_probe_kernel, dim3(256), dim3(512), 0, (hipStream_t)stream, (int)mode, (int)iters,
+                       (const uint8_t*)src, out);
+    return hipGetLastError() == hipSuccess ? 0 : 3;
+}
 
 int32_t fp8probe_stream(const void* src, int64_t n, void* dst1, void* dst2, void* stream) {
     if (n < 8 || n % 8 || !src || !dst1 || ((uintptr_t)src % 16) || ((uintptr_t)dst1 % 8) ||

@@ -307,3 +307,32 @@ def test_quantise_batch_rejects(L):
     assert call([args()], fmt=4) == F.EINVAL
     assert call([args()], margin=1 << 20) == F.EINVAL
     assert F.QUANTISE_BATCH_MAX == 4 and "FP8_QUANTISE_BATCH_MAX 4" in open(HEADER).read()
+
+
+PROBE_HEADER = os.path.join(ROOT, "include", "fp8probe.h")
+
+
+def test_probe_library_exports_and_rejects():
+    """The measurement aid libfp8probe.so (include/fp8probe.h): every declared
+    function is exported, and bad arguments are rejected before any launch."""
+    from paper_2309_17224_amd import build
+    if not os.path.exists(build.PROBE_LIB):
+        build.build()
+    P = ctypes.CDLL(build.PROBE_LIB)
+    text = re.sub(r"/\*.*?\*/", "", open(PROBE_HEADER).read(), flags=re.S)
+    names = set(re.findall(r"^\s*[a-z_0-9]+\s*\*?\s*([a-z_0-9]+)\s*\(", text, re.M))
+    assert names == {"fp8probe_mfma_loop_flops", "fp8probe_mfma_loop", "fp8probe_stream",
+                     "fp8probe_lds_src_bytes", "fp8probe_lds"}
+    for n in names:
+        assert hasattr(P, n), n
+    P.fp8probe_lds_src_bytes.restype = ctypes.c_int64
+    assert P.fp8probe_lds_src_bytes() == 64 << 20
+    P.fp8probe_lds.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    assert P.fp8probe_lds(4, 10, FAKE, FAKE, NULL) == 1      # unknown mode
+    assert P.fp8probe_lds(0, 0, FAKE, FAKE, NULL) == 1       # no iterations
+    assert P.fp8probe_lds(0, 10, NULL, FAKE, NULL) == 1      # no source
+    assert P.fp8probe_lds(0, 10, A8, FAKE, NULL) == 1        # source not 16-byte aligned
+    P.fp8probe_stream.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    assert P.fp8probe_stream(FAKE, 12, FAKE, NULL, NULL) == 1  # n not a multiple of 8
+    P.fp8probe_mfma_loop.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    assert P.fp8probe_mfma_loop(0, 10, 1, FAKE, NULL) == 1   # no workgroups
