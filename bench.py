@@ -94,7 +94,8 @@ def parse(argv=None):
                    help="time the LDS read / LDS-copy probe of libfp8probe.so (ITERS loop trips) and exit")
     p.add_argument("--stream-ceiling", type=int, default=0, metavar="MB",
                    help="only run the cast-shaped stream of libfp8probe.so on a bf16 tensor of MB megabytes "
-                        "(2 bytes read, 1 or 2 written per element), --steps launches each, then exit")
+                        "(2 bytes read, 1 or 2 written per element; a read + write reference rate), --steps "
+                        "launches each, then exit")
     p.add_argument("--no-configs", action="store_true",
                    help="time the chosen workload only (no table of the other workloads)")
     p.add_argument("--no-mispredicted", action="store_true",
@@ -460,12 +461,14 @@ def quantise_table(step, per_call):
 
 
 def stream_ceilings(mb=1024, launches=5):
-    """Measured read + write ceilings of a cast-shaped stream (libfp8probe.so):
-    GB/s for 2 bytes read + 1 written and 2 read + 2 written per element."""
+    """Read + write rates of a cast-shaped stream (libfp8probe.so): GB/s for
+    2 bytes read + 1 written and 2 read + 2 written per element.  A reference
+    measured in the same run, not a bound: the tiled quantise passes exceed it
+    on some tensors."""
     import ctypes
     import torch
     P = probe_lib()
-    n = (mb << 20) // 2 // 8 * 8
+    n = (mb << 20) // 2 // 16 * 16
     src = torch.zeros(n, dtype=torch.bfloat16, device="cuda")
     d1 = torch.empty(n, dtype=torch.uint8, device="cuda")
     d2 = torch.empty(n, dtype=torch.uint8, device="cuda")
@@ -642,13 +645,13 @@ def lds_probe(args):
 
 
 def stream_ceiling(args):
-    """Read + write ceiling of a cast-shaped stream (measurement aid
+    """Read + write rate of a cast-shaped stream (measurement aid
     libfp8probe.so): 2 bytes read and 1 (codes) or 2 (codes and a second
     copy) written per element, HIP events around each launch."""
     import ctypes
     import torch
     P = probe_lib()
-    n = (args.stream_ceiling << 20) // 2 // 8 * 8
+    n = (args.stream_ceiling << 20) // 2 // 16 * 16
     src = torch.randn(n, dtype=torch.float32, device="cuda").to(torch.bfloat16)
     d1 = torch.empty(n, dtype=torch.uint8, device="cuda")
     d2 = torch.empty(n, dtype=torch.uint8, device="cuda")
@@ -759,7 +762,7 @@ def main(argv=None):
         return
     w = wl.WORKLOADS[args.workload]
     ceil = stream_ceilings()
-    log(f"[bench] cast-shaped stream ceilings (GB/s): {ceil}")
+    log(f"[bench] cast-shaped stream reference (GB/s): {ceil}")
     res = bench_workload(args, w, args.steps, args.warmup,
                          cpu_baseline_budget=None if args.no_cpu_baseline else args.cpu_budget,
                          mispredicted=not args.no_mispredicted)
@@ -769,13 +772,16 @@ def main(argv=None):
            "vs_baseline": None, "dtype": "fp8", "data": "synthetic", "config": res.pop("config")}
     out.update(res)
     out.setdefault("cpu_baseline", None)
-    # every quantise call against HBM peak (3 bytes per element) and against the
-    # measured ceiling of a stream with the same bytes read and written
-    out["quantise_ceiling_GBps"] = {**ceil, "source": "libfp8probe.so stream, 1 GiB bf16, HIP events"}
+    # every quantise call against HBM peak (3 bytes per element) and against a
+    # stream with the same bytes read and written, measured in the same run
+    out["stream_reference_GBps"] = {
+        **ceil, "source": "libfp8probe.so cast-shaped stream (contiguous range per workgroup, no arithmetic), "
+                          "1 GiB bf16, HIP events; a reference, not a bound: tiled quantise passes exceed it "
+                          "on some tensors"}
     for q in out.get("quantise_calls", []):
         wr2 = q["transpose_bytes"] > 0
         c = ceil["read2_write2"] if wr2 else ceil["read2_write1"]
-        q["frac_of_ceiling"] = round(q["GB_per_s_incl_transpose" if wr2 else "GB_per_s"] / c, 4)
+        q["vs_stream_reference"] = round(q["GB_per_s_incl_transpose" if wr2 else "GB_per_s"] / c, 4)
     if not args.no_configs and args.workload == DEFAULT_WORKLOAD:
         side = {}
         for name in SIDE_WORKLOADS:

@@ -14,10 +14,10 @@
  * per instruction).
  *
  * fp8probe_stream -- the memory traffic of a cast with no arithmetic: reads n
- * bf16 elements of src (device, 16-byte aligned, n a multiple of 8) and writes
- * one byte per element to dst1 and, if dst2 is not NULL, one more to dst2
- * (device, 8-byte aligned): 3 or 4 bytes per element, each workgroup a
- * contiguous range, non-temporal loads and stores.  Returns as above.
+ * bf16 elements of src (device, 16-byte aligned, n a multiple of 16) and
+ * writes one byte per element to dst1 and, if dst2 is not NULL, one more to
+ * dst2 (device, 16-byte aligned): 3 or 4 bytes per element, each workgroup a
+ * contiguous range, 16-byte non-temporal loads and stores.  Returns as above.
  *
  * fp8probe_lds -- LDS traffic of the matmul's main loop in isolation: 256
  * workgroups of 8 waves, each wave iters x 8 ds_read_b128 of 1 KiB and/or

@@ -66,35 +66,39 @@ __global__ __launch_bounds__(512) void mfma_loop_kernel(int iters, uint32_t seed
 }
 
 // Cast-shaped stream: each workgroup reads one contiguous range of bf16
-// elements with eight 16-byte non-temporal loads in flight per lane and
-// writes one byte per element (the high byte of each bf16: no conversion
-// arithmetic) to dst1 and, if given, to dst2, with non-temporal stores.
-constexpr int kStreamThreads = 256, kStreamL = 8;
+// elements, sixteen per lane and step (two 16-byte non-temporal loads), with
+// four such groups (eight loads) in flight per lane, and writes one byte per
+// element (the high byte of each bf16: no conversion arithmetic) as one
+// 16-byte non-temporal store per group to dst1 and, if given, to dst2.
+constexpr int kStreamThreads = 256, kStreamG = 4;
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
-__global__ __launch_bounds__(kStreamThreads) void stream_kernel(const u32x4* __restrict__ src, int64_t nv,
-                                                                 u32x2* __restrict__ dst1, u32x2* __restrict__ dst2) {
-    const int64_t chunk = ((nv + gridDim.x - 1) / gridDim.x + 255) & ~(int64_t)255;
-    const int64_t b0 = min(nv, (int64_t)blockIdx.x * chunk), b1 = min(nv, b0 + chunk);
-    for (int64_t i = b0 + threadIdx.x; i < b1; i += kStreamL * kStreamThreads) {
-        u32x4 v[kStreamL];
+__device__ __forceinline__ uint32_t high_bytes(uint32_t a, uint32_t b) {
+    return ((a >> 8) & 0xFFu) | ((a >> 16) & 0xFF00u) | ((b << 8) & 0xFF0000u) | (b & 0xFF000000u);
+}
+
+__global__ __launch_bounds__(kStreamThreads) void stream_kernel(const u32x4* __restrict__ src, int64_t ng,
+                                                                 u32x4* __restrict__ dst1, u32x4* __restrict__ dst2) {
+    // ng groups of 16 elements = 2 source vectors and 1 destination vector each
+    const int64_t chunk = ((ng + gridDim.x - 1) / gridDim.x + 255) & ~(int64_t)255;
+    const int64_t b0 = min(ng, (int64_t)blockIdx.x * chunk), b1 = min(ng, b0 + chunk);
+    for (int64_t i = b0 + threadIdx.x; i < b1; i += kStreamG * kStreamThreads) {
+        u32x4 v[2 * kStreamG];
 #pragma unroll
-        for (int l = 0; l < kStreamL; ++l) {
+        for (int l = 0; l < kStreamG; ++l) {
             const int64_t j = min(i + l * kStreamThreads, b1 - 1);
-            v[l] = __builtin_nontemporal_load(src + j);
+            v[2 * l] = __builtin_nontemporal_load(src + 2 * j);
+            v[2 * l + 1] = __builtin_nontemporal_load(src + 2 * j + 1);
         }
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int l = 0; l < kStreamL; ++l) {
+        for (int l = 0; l < kStreamG; ++l) {
             const int64_t j = i + l * kStreamThreads;
             if (j < b1) {
-                const uint32_t lo = ((v[l].x >> 8) & 0xFFu) | ((v[l].x >> 16) & 0xFF00u) | ((v[l].y << 8) & 0xFF0000u) |
-                                    (v[l].y & 0xFF000000u);
-                const uint32_t hi = ((v[l].z >> 8) & 0xFFu) | ((v[l].z >> 16) & 0xFF00u) | ((v[l].w << 8) & 0xFF0000u) |
-                                    (v[l].w & 0xFF000000u);
-                __builtin_nontemporal_store(u32x2{lo, hi}, dst1 + j);
-                if (dst2) __builtin_nontemporal_store(u32x2{hi, lo}, dst2 + j);
+                const u32x4 a = v[2 * l], b = v[2 * l + 1];
+                const u32x4 c = {high_bytes(a.x, a.y), high_bytes(a.z, a.w), high_bytes(b.x, b.y), high_bytes(b.z, b.w)};
+                __builtin_nontemporal_store(c, dst1 + j);
+                if (dst2) __builtin_nontemporal_store(u32x4{c.y, c.x, c.w, c.z}, dst2 + j);
             }
         }
     }
@@ -165,11 +169,11 @@ int32_t fp8probe_lds(int32_t mode, int32_t iters, const void* src, uint32_t* out
 }
 
 int32_t fp8probe_stream(const void* src, int64_t n, void* dst1, void* dst2, void* stream) {
-    if (n < 8 || n % 8 || !src || !dst1 || ((uintptr_t)src % 16) || ((uintptr_t)dst1 % 8) ||
-        (dst2 && ((uintptr_t)dst2 % 8)))
+    if (n < 16 || n % 16 || !src || !dst1 || ((uintptr_t)src % 16) || ((uintptr_t)dst1 % 16) ||
+        (dst2 && ((uintptr_t)dst2 % 16)))
         return 1;
     hipLaunchKernelGGL(stream_kernel, dim3(2048), dim3(kStreamThreads), 0, (hipStream_t)stream, (const u32x4*)src,
-                       n / 8, (u32x2*)dst1, (u32x2*)dst2);
+                       n / 16, (u32x4*)dst1, (u32x4*)dst2);
     return hipGetLastError() == hipSuccess ? 0 : 3;
 }
 

@@ -333,6 +333,6 @@ def test_probe_library_exports_and_rejects():
     assert P.fp8probe_lds(0, 10, NULL, FAKE, NULL) == 1      # no source
     assert P.fp8probe_lds(0, 10, A8, FAKE, NULL) == 1        # source not 16-byte aligned
     P.fp8probe_stream.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
-    assert P.fp8probe_stream(FAKE, 12, FAKE, NULL, NULL) == 1  # n not a multiple of 8
+    assert P.fp8probe_stream(FAKE, 24, FAKE, NULL, NULL) == 1  # n not a multiple of 16
     P.fp8probe_mfma_loop.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
     assert P.fp8probe_mfma_loop(0, 10, 1, FAKE, NULL) == 1   # no workgroups
