@@ -57,11 +57,14 @@ def parse(argv=None):
                    help="write this many MB before every step (evicts the 256 MB MALL), and in the "
                         "per-call pass also before every decode matmul (weights from HBM, as in "
                         "token-by-token decode)")
-    p.add_argument("--quant", choices=("predicted", "twopass", "separate", "cscale"), default="predicted",
+    p.add_argument("--quant", choices=("predicted", "twopass", "separate", "delayed", "cscale"), default="predicted",
                    help="bias + cast of X, W, dY: one fp8_quantise call predicting each bias from "
                         "the previous step (identical bits; one read of an unchanged tensor), "
-                        "fp8_quantise without prediction, fp8_scale_bias + fp8_cast, or FP8-CSCALE "
-                        "(constant bias --cscale-bias, no amax: not the headline metric)")
+                        "fp8_quantise without prediction, fp8_scale_bias + fp8_cast, delayed scaling "
+                        "(fp8_quantise_delayed: Eq. 3 of the largest amax of the last --history-len steps, "
+                        "never re-cast: other bits than the just-in-time modes), or FP8-CSCALE "
+                        "(constant bias --cscale-bias, no amax); the last two are not the headline metric")
+    p.add_argument("--history-len", type=int, default=16, help="amax history length of --quant delayed")
     p.add_argument("--cscale-bias", type=int, default=0)
     p.add_argument("--streams", type=int, choices=(1, 2), default=1,
                    help="graph of the timed steps: independent calls (input quantises, gradient "
@@ -110,7 +113,7 @@ def step_kwargs(args) -> dict:
     with these, so that the benchmark times the configuration they check)."""
     return dict(margin=args.margin, quant=args.quant, cscale_bias=args.cscale_bias,
                 fused_bias=args.bias == "fused", concurrent=args.streams == 2,
-                batch_quant=not args.no_quant_batch)
+                batch_quant=not args.no_quant_batch, history_len=args.history_len)
 
 
 def log(msg):
@@ -556,6 +559,7 @@ def bench_workload(args, w, steps, warmup, cpu_baseline_budget=None, mispredicte
                    "mode": "train fwd+bwd" if w.train else "PTQ inference fwd",
                    "accumulate": "fp32", "outputs": "Y,dX bf16; dW fp32" if w.train else "Y bf16",
                    "margin": args.margin, "mall_flush_mb": args.flush_mb, "quant": args.quant,
+                   "history_len": args.history_len if args.quant == "delayed" else None,
                    "quant_batch": not args.no_quant_batch, "output_bias": args.bias,
                    "launch": (f"one HIP graph replay per step, {args.streams} stream(s)" if args.launch == "graph"
                               else "one host call per library call"),
