@@ -114,7 +114,7 @@ size_t fp8_scale_bias_ws_bytes(int64_t n);
  * ws:        device workspace of at least fp8_scale_bias_ws_bytes(n) bytes,
  *            4-byte aligned; its contents are scratch.  Concurrent calls need
  *            distinct workspaces.
- * n == 0 gives amax 0, bias 0 and FP8_FLAG_ZERO.
+ * n == 0 gives amax 0, bias 0 and FP8_FLAG_ZERO; n above 2^46 is FP8_EINVAL.
  */
 int32_t fp8_scale_bias(const void *x, int32_t dt, int64_t n, int32_t fmt, int32_t margin,
                        int32_t *bias, uint32_t *amax_bits, uint32_t *flags,
@@ -141,7 +141,8 @@ int32_t fp8_bias_from_amax(const uint32_t *amax_bits, int32_t fmt, int32_t margi
  * qT:   out, optional, the same codes transposed: [cols, rows], row stride
  *       ldqT >= rows.  The matmuls below take this copy where they contract
  *       over the rows of a tensor.
- * rows == 0 or cols == 0 is a no-op.
+ * rows == 0 or cols == 0 is a no-op.  A tensor of more than INT32_MAX tiles
+ * of 128 x 128 (one workgroup each) returns FP8_ENOTSUP.
  */
 int32_t fp8_cast_e4(const void *x, int32_t dt, int64_t rows, int64_t cols, int64_t ldx,
                     const int32_t *bias, uint8_t *q, int64_t ldq, uint8_t *qT, int64_t ldqT,
@@ -436,6 +437,7 @@ int32_t fp8_linear_bwd_dw(const uint8_t *x8t, const int32_t *bx, const uint8_t *
  *      At least one of w8 / w8t must be given.
  * bw:  out, the weight's bias (device).  flags: optional, as fp8_scale_bias.
  * ws:  workspace of fp8_scale_bias_ws_bytes(K * N) bytes.
+ * K * N above the element count fp8_scale_bias accepts (2^46) is FP8_EINVAL.
  */
 int32_t ptq_quantise_weights(const void *w, int32_t dt, int64_t K, int64_t N, uint8_t *w8,
                              uint8_t *w8t, int32_t *bw, uint32_t *flags, void *ws,

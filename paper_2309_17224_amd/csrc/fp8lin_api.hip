@@ -26,6 +26,7 @@ int32_t cast_common(const void* x, int32_t dt, int64_t rows, int64_t cols, int64
     if (!x || !bias || (!q && !qT)) return FP8_EINVAL;
     if (!aligned(x, esize(dt)) || !aligned(bias, 4)) return FP8_EINVAL;
     if (ldx < cols || (q && ldq < cols) || (qT && ldqT < rows)) return FP8_EINVAL;
+    if (quantise_tiles_upto(rows, cols, INT32_MAX) < 0) return FP8_ENOTSUP;  // one workgroup per 128 x 128 tile
     return launch_cast(x, dt, rows, cols, ldx, fmt, bias, q, ldq, qT, ldqT, as_stream(stream));
 }
 
@@ -475,6 +476,7 @@ int32_t ptq_quantise_weights(const void* w, int32_t dt, int64_t K, int64_t N, ui
                              uint8_t* w8t, int32_t* bw, uint32_t* flags, void* ws, size_t ws_bytes,
                              void* stream) {
     if (!dt_ok(dt) || K < 0 || N < 0 || K > kMaxDim || N > kMaxDim) return FP8_EINVAL;
+    if (N > 0 && K > kMaxDim * 64 / N) return FP8_EINVAL;  // K * N beyond what fp8_scale_bias accepts
     if (!bw || (!w8 && !w8t)) return FP8_EINVAL;
     int32_t st = fp8_scale_bias(w, dt, K * N, FP8_E4M3, 0, bw, nullptr, flags, ws, ws_bytes, stream);
     if (st != FP8_OK || K == 0 || N == 0) return st;

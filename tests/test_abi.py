@@ -80,6 +80,8 @@ def test_cast_rejects(L):
         assert f(ODD, 0, 4, 8, 8, FAKE, FAKE, 8, NULL, 4, NULL) == F.EINVAL    # alignment
         assert f(FAKE, 0, -4, 8, 8, FAKE, FAKE, 8, NULL, 4, NULL) == F.EINVAL  # rows < 0
         assert f(NULL, 0, 0, 8, 8, NULL, NULL, 8, NULL, 4, NULL) == F.OK       # empty: no-op
+        big = 1 << 39  # 2^32 x 2^32 tiles of 128 x 128: more workgroups than one launch holds
+        assert f(FAKE, 0, big, big, big, FAKE, FAKE, big, NULL, big, NULL) == F.ENOTSUP
 
 
 def test_quantise_workspace_size(L):
@@ -145,6 +147,9 @@ def test_ptq_and_bias_from_amax_reject(L):
     assert L.ptq_quantise_weights(FAKE, 0, 4, 4, NULL, NULL, FAKE, NULL, FAKE, 64, NULL) == F.EINVAL
     assert L.ptq_quantise_weights(FAKE, 0, 4, 4, FAKE, NULL, NULL, NULL, FAKE, 64, NULL) == F.EINVAL
     assert L.ptq_quantise_weights(FAKE, 9, 4, 4, FAKE, NULL, FAKE, NULL, FAKE, 64, NULL) == F.EINVAL
+    # K * N past the element count an amax call accepts (2^46), including products past 2^63
+    assert L.ptq_quantise_weights(FAKE, 0, 1 << 24, 1 << 23, FAKE, NULL, FAKE, NULL, FAKE, 64, NULL) == F.EINVAL
+    assert L.ptq_quantise_weights(FAKE, 0, 1 << 33, 1 << 33, FAKE, NULL, FAKE, NULL, FAKE, 64, NULL) == F.EINVAL
     assert L.fp8_bias_from_amax(NULL, 0, 0, FAKE, NULL, NULL) == F.EINVAL
     assert L.fp8_bias_from_amax(FAKE, 5, 0, FAKE, NULL, NULL) == F.EINVAL
     assert L.fp8_bias_from_amax(FAKE, 0, 0, ODD, NULL, NULL) == F.EINVAL
