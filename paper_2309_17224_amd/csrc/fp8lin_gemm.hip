@@ -12,12 +12,15 @@
 //    of v_mfma_f32_16x16x128_f8f6f4; the two waves of a SIMD own the two
 //    halves of one 128 x 128 quadrant.
 //  * K advances 128 bytes at a time; both operand tiles (256 rows x 128 B)
-//    go HBM/L2 -> LDS with global_load_lds_dwordx4 (no VGPR staging) into a
-//    double buffer (2 x 64 KiB).
+//    go HBM/L2 -> LDS with global_load_lds_dwordx4 (no VGPR staging): A into
+//    two stages, B into three (all 160 KiB of LDS).
+//  * The copies are slow to issue (the L1 holds only so many outstanding
+//    fills): group 0 copies the A tiles and group 1 the B tiles, each in its
+//    own load phase, so both load phases share the cost.
 //  * The two waves of a SIMD alternate between an MFMA phase and a load
 //    phase, the phases separated by workgroup barriers: while one issues its
 //    32 MFMAs of step k, the other reads all its fragments of its next step
-//    into registers (and, in group 0, issues the copies of a later step).
+//    into registers and issues the copies of its operand for a later step.
 //    The matrix core of each SIMD is fed by one wave at a time, and the
 //    cost of issuing vector-memory and LDS instructions falls on the wave
 //    that is not feeding it (see the main loop).
@@ -211,8 +214,13 @@ __device__ __forceinline__ void st_stream(void* p, uint4 v) {
 constexpr int kEpRowBf16 = 128 * 2 + 16, kEpRowF32 = 128 * 4 + 16;
 constexpr int kEpBf16Bytes = 8 * 32 * kEpRowBf16, kEpF32Bytes = 8 * 32 * kEpRowF32;
 constexpr int kCodesOff = kEpBf16Bytes;
-constexpr int kSmemBytes = kCodesOff + kBM * kBN > kEpF32Bytes ? kCodesOff + kBM * kBN : kEpF32Bytes;
-static_assert(kSmemBytes >= 2 * 2 * kTileBytes && kSmemBytes <= 160 * 1024, "LDS budget");
+constexpr int kEpBytes = kCodesOff + kBM * kBN > kEpF32Bytes ? kCodesOff + kBM * kBN : kEpF32Bytes;
+// Main loop: two A stages and three B stages (B tiles are copied two steps
+// ahead, see gemm_tile); the epilogue reuses the space, and the workgroup's
+// amax words sit in its last 64 bytes, past every epilogue staging area.
+constexpr int kSmemBytes = 2 * kTileBytes + 3 * kBN * kBK;
+constexpr int kWmxOff = kSmemBytes - 64;
+static_assert(kEpBytes <= kWmxOff && kSmemBytes <= 160 * 1024, "LDS budget");
 static_assert(kCodesOff % 16 == 0, "codes staging alignment");
 
 // Output codes of the fused quantise (QF >= 0, bf16 output only): Y8 [M, N]
@@ -265,7 +273,7 @@ __device__ __forceinline__ void gemm_tile(
     static_assert(QF < 0 || TN == 256, "fused quantise stages whole 256 x 256 tiles");
     static_assert(TN % 64 == 0 && TN >= 64 && TN <= 256, "tile width");
     constexpr int kNbw = TN / 32;                  // 16-column blocks per wave, B copies per loader wave
-    constexpr int kStage = kTileBytes + TN * kBK;  // A tile + B tile
+    constexpr int kBStage = TN * kBK;              // one B tile in LDS
     constexpr int kNf = 4 + kNbw;                  // fragment pieces a wave reads per step
     constexpr int kNc = 8 + kNbw;                  // copies a loader wave issues per stage
 
@@ -299,11 +307,12 @@ __device__ __forceinline__ void gemm_tile(
     const uint8_t* baseB = B + (int64_t)n0 * K;
     // LDS addresses of this wave's first loader rows (wave-uniform); copy d
     // < 8 fills A row group d, copy d >= 8 B row group d - 8.
+    // LDS: A stages 0 and 1 at s * kTileBytes, B stages 0, 1 and 2 after them.
     const uint32_t lds_a = __builtin_amdgcn_readfirstlane(lds_addr(smem) + sq * 64 * kBK);
-    const uint32_t lds_b = __builtin_amdgcn_readfirstlane(lds_addr(smem) + kTileBytes + sq * (TN / 4) * kBK);
-    auto dma = [&](int d, int stage, int k0) {
+    const uint32_t lds_b = __builtin_amdgcn_readfirstlane(lds_addr(smem) + 2 * kTileBytes + sq * (TN / 4) * kBK);
+    auto dma = [&](int d, int stage, int k0) {  // stage: of A for d < 8, of B for d >= 8
         lds_dma16_s((d >= 8 ? baseB : baseA) + k0, voff[d],
-                    (d >= 8 ? lds_b + (d - 8) * 8 * kBK : lds_a + d * 8 * kBK) + stage * kStage);
+                    d >= 8 ? lds_b + (d - 8) * 8 * kBK + stage * kBStage : lds_a + d * 8 * kBK + stage * kTileBytes);
     };
 
     // this wave's sub-tile: rows [wr0, wr0 + 64), columns [wc0, wc0 + TN/2) of the tile
@@ -324,43 +333,67 @@ __device__ __forceinline__ void gemm_tile(
     //   phase 1:        group 0 loads fragments of step 0
     //   phase 2k + 2:   group 0 MFMAs of step k,   group 1 loads step k
     //   phase 2k + 3:   group 0 loads step k + 1,  group 1 MFMAs of step k
-    // A load phase reads all 24 fragment pieces of the wave's next step and
-    // waits for them before the barrier.  Tile k sits in buffer k % 2; group 0
-    // copies tile k + 1 into the other buffer in its load phase of step k
-    // (tiles 0 and 1 before phase 1), after both groups have read tile k - 1
-    // from it, and waits for those copies at the end of its next MFMA phase,
-    // before either group reads tile k + 1.  Every wave passes 2 nk + 1
+    // A load phase reads all kNf fragment pieces of the wave's next step and
+    // waits for them before the barrier.  A tile k sits in A stage k % 2, B
+    // tile k in B stage k % 3.  Group 0 copies A tile k + 1 in its load phase
+    // of step k (after both groups have read A tile k - 1 from that stage) and
+    // waits for the copies at the end of its next MFMA phase.  Group 1 copies
+    // B tile k + 2 in its load phase of step k (B tile k - 1 has been read by
+    // then) and, before that phase's barrier, waits for B tile k + 1 — issued
+    // one load phase earlier — but not for the copies it has just issued.
+    // Steps 0 and 1 are copied before phase 1.  Every wave passes 2 nk + 1
     // barriers (group 1 passes one before its first load phase and none after
     // its last MFMA phase), so the groups stay in step.
     const int nk = K / kBK;
-    if (g == 0 && nk > 0) {
-#pragma unroll
-        for (int d = 0; d < kNc; ++d) dma(d, 0, 0);
-        if (nk > 1) {
-#pragma unroll
-            for (int d = 0; d < kNc; ++d) dma(d, 1, kBK);
-            wait_vmcnt<kNc>();
-        } else {
-            wait_vmcnt<0>();
-        }
-    }
     if (nk > 0) {
+        if (g == 0) {
+#pragma unroll
+            for (int d = 0; d < 8; ++d) dma(d, 0, 0);
+            if (nk > 1) {
+#pragma unroll
+                for (int d = 0; d < 8; ++d) dma(d, 1, kBK);
+                wait_vmcnt<8>();
+            } else {
+                wait_vmcnt<0>();
+            }
+        } else {
+#pragma unroll
+            for (int d = 8; d < kNc; ++d) dma(d, 0, 0);
+            if (nk > 1) {
+#pragma unroll
+                for (int d = 8; d < kNc; ++d) dma(d, 1, kBK);
+                wait_vmcnt<kNbw>();
+            } else {
+                wait_vmcnt<0>();
+            }
+        }
         ws_barrier();
         if (g == 1) ws_barrier();
     }
     v8i af[4], bf[kNbw];
+    int bs = 0;  // k % 3: the B stage of step k
     for (int kt = 0; kt < nk; ++kt) {
-        const uint8_t* sa = smem + (kt & 1) * kStage + wr0 * kBK;
-        const uint8_t* sb = smem + (kt & 1) * kStage + kTileBytes + wc0 * kBK;
+        const uint8_t* sa = smem + (kt & 1) * kTileBytes + wr0 * kBK;
+        const uint8_t* sb = smem + 2 * kTileBytes + bs * kBStage + wc0 * kBK;
         if (g == 0 && kt >= 1 && kt + 1 < nk) {
+            // A tile of step kt + 1, the copies spread over the fragment reads
             const int st = (kt + 1) & 1, k1 = (kt + 1) * kBK;
-            // kNc = kNf + 4 copies spread over the kNf fragment reads
 #pragma unroll
             for (int q = 0; q < kNf; ++q) {
                 if (q < 4) af[q] = ld_frag(sa + q * 16 * kBK, fo0, fo1);
                 else bf[q - 4] = ld_frag(sb + (q - 4) * 16 * kBK, fo0, fo1);
-                dma(q, st, k1);
-                if (q < 4) dma(kNf + q, st, k1);
+                if (q < 8) dma(q, st, k1);
+            }
+#pragma unroll
+            for (int d = kNf; d < 8; ++d) dma(d, st, k1);
+        } else if (g == 1 && kt + 2 < nk) {
+            // B tile of step kt + 2 into the stage B tile kt - 1 used
+            const int st = bs == 0 ? 2 : bs - 1, k2 = (kt + 2) * kBK;
+#pragma unroll
+            for (int q = 0; q < kNf; ++q) {
+                if (q < 4) af[q] = ld_frag(sa + q * 16 * kBK, fo0, fo1);
+                else bf[q - 4] = ld_frag(sb + (q - 4) * 16 * kBK, fo0, fo1);
+                if (q < kNbw) dma(8 + q, st, k2);
             }
         } else {
 #pragma unroll
@@ -369,6 +402,11 @@ __device__ __forceinline__ void gemm_tile(
                 else bf[q - 4] = ld_frag(sb + (q - 4) * 16 * kBK, fo0, fo1);
             }
         }
+        if (g == 1) {  // B tile kt + 1 has landed (the copies just issued need not have)
+            if (kt + 2 < nk) wait_vmcnt<kNbw>();
+            else wait_vmcnt<0>();
+        }
+        bs = bs == 2 ? 0 : bs + 1;
         wait_lgkmcnt0();
         ws_barrier();
 #pragma unroll
@@ -545,7 +583,7 @@ __device__ __forceinline__ void gemm_tile(
         // on one word from every wave would queue behind each other).  Rows
         // and columns past the edge computed clamped copies of real ones, so
         // including them cannot change the maximum.
-        __shared__ uint32_t wmx[kMainThreads / 64];
+        uint32_t* wmx = (uint32_t*)(smem + kWmxOff);
         const uint32_t wv = wave_max_u32(mx);
         if (lane == 0) wmx[w] = wv;
         __syncthreads();
