@@ -292,8 +292,10 @@ __global__ __launch_bounds__(kThreads) void swiglu_kernel(
 //                  each lane holds S^T[4 keys][1 query] per 16 x 16 tile;
 //   O^T += V^T . P^T: B = the probabilities straight from the S^T registers
 //                  (keys 4g..4g+3 and 16+4g..16+4g+3 of a 32-key slice for
-//                  lane group g), A = V^T read from an LDS copy of V stored
-//                  transposed with the keys of each slice permuted to match.
+//                  lane group g), A = V^T fragments taken from the row-major
+//                  LDS copy of V by gfx950's transposing LDS read
+//                  (ds_read_b64_tr_b16), which hands each lane one column of
+//                  four consecutive keys, in the key order of P.
 // Online softmax in fp32 with base-2 exponentials (the scale log2(e) /
 // sqrt(128) folded into the exponent's FMA); the exponent offset follows the
 // running maximum lazily (moved only when it is exceeded by 8 in log2 units,
@@ -359,9 +361,21 @@ __device__ __forceinline__ float quad_sum(float v) {
     return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
-// Placement of row d of the transposed V block (see the attention kernel).
-__device__ __forceinline__ int vt_row(int d) { return d ^ ((d >> 5) & 1); }
-__device__ __forceinline__ int vt_swz(int d) { return ((d >> 1) ^ (d >> 3)) & 7; }
+// Physical 16-byte chunk of logical chunk c in LDS row `key` of a V block:
+// c ^ v_swz(key), which moves whole 32-byte chunk pairs.  A transposing read
+// (below) takes 32 contiguous bytes of each of 8 consecutive keys per half
+// wave; keys differing in bits 0-2 then sit in different pairs, so each half
+// wave reads all 64 banks once.
+__device__ __forceinline__ int v_swz(int key) { return 2 * (key & 7); }
+
+// ds_read_b64_tr_b16: within each group of 16 lanes, lane 4a + b receives
+// element b of the 8-byte chunks addressed by lanes a, 4 + a, 8 + a and
+// 12 + a (measured on gfx950 with index patterns).
+typedef short v4s_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint2 lds_read_tr16(const uint8_t* p) {
+    const v4s_t r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s_t*)p);
+    return __builtin_bit_cast(uint2, r);
+}
 
 template <bool QUANT, int FMT>
 __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
@@ -407,74 +421,39 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
         for (int ds = 0; ds < 4; ++ds) qf[qt][ds] = ldg16(Qg + (int64_t)row * p.ld + 32 * ds + 8 * g);
     }
 
-    // Staging roles: K goes straight to LDS, wave w copying keys 16 w .. 16 w + 15
-    // (4 copies of 4 rows; lane l: key 16 w + 4 j + l/16, physical chunk l%16,
-    // which holds logical chunk (l%16) ^ (key mod 16)); V goes through
-    // registers, keys 4u .. 4u+3 x columns 8v .. 8v+7 (u = tid/16, v = tid%16).
-    // Rows past kend read row kend-1 (a finite copy; those keys are masked).
-    // Full blocks: a wave-uniform block base plus per-lane 32-bit offsets; the
-    // last, partial block clamps each row.
-    const int vu = w + 4 * ((tid >> 4) & 3), vv = tid & 15;
+    // Staging: K and V go straight to LDS (global_load_lds_dwordx4), wave w
+    // copying keys 16 w .. 16 w + 15 of each (4 copies of 4 rows; lane l: key
+    // 16 w + 4 j + l/16, physical chunk l%16, which holds logical chunk
+    // (l%16) ^ (key mod 16) for K and (l%16) ^ v_swz(key) for V).  Both are
+    // rows of 256 bytes, one per key.  Rows past kend read row kend-1 (a
+    // finite copy; those keys are masked).  Full blocks: a wave-uniform block
+    // base plus per-lane 32-bit offsets; the last, partial block clamps each
+    // row.
     const int ld = (int)p.ld;
-    const int voff = 4 * vu * ld + 8 * vv;
     const int wu = __builtin_amdgcn_readfirstlane(w);
     int kkey[4];
-    uint32_t kboff[4];  // byte offsets of this lane's K copies in a full block
+    uint32_t kboff[4], vboff[4];  // byte offsets of this lane's K and V copies in a full block
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
         kkey[j] = 16 * wu + 4 * j + (lane >> 4);
         kboff[j] = (uint32_t)(kkey[j] * ld + 8 * ((lane & 15) ^ (kkey[j] & 15))) * 2u;
+        vboff[j] = (uint32_t)(kkey[j] * ld + 8 * ((lane & 15) ^ v_swz(kkey[j]))) * 2u;
     }
-    u32x4 vreg[4];
-    auto copy_k = [&](int kb, int buf) {
+    // One block of K (V = false) or V into buffer buf.
+    auto copy_kv = [&](int kb, int buf, bool V) {
         const int kbase = kb * kBk;
-        const uint16_t* kp = Kg + (int64_t)kbase * p.ld;
-        const uint32_t dst = lds_addr32(lds + buf * 2 * kKvBytes) + (16 * wu) * 256;
+        const uint16_t* src = (V ? Vg : Kg) + (int64_t)kbase * p.ld;
+        const uint32_t dst = lds_addr32(lds + buf * 2 * kKvBytes + (V ? kKvBytes : 0)) + (16 * wu) * 256;
         if (kbase + kBk <= kend) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) lds_copy16(kp, kboff[j], dst + j * 1024);
+            for (int j = 0; j < 4; ++j) lds_copy16(src, V ? vboff[j] : kboff[j], dst + j * 1024);
         } else {
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int row = min(kbase + kkey[j], kend - 1) - kbase;
-                lds_copy16(kp, (uint32_t)(row * ld + 8 * ((lane & 15) ^ (kkey[j] & 15))) * 2u, dst + j * 1024);
+                const int c = (lane & 15) ^ (V ? v_swz(kkey[j]) : (kkey[j] & 15));
+                lds_copy16(src, (uint32_t)(row * ld + 8 * c) * 2u, dst + j * 1024);
             }
-        }
-    };
-    auto load_v = [&](int kb) {
-        const int kbase = kb * kBk;
-        const uint16_t* vp = Vg + (int64_t)kbase * p.ld;
-        if (kbase + kBk <= kend) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) vreg[j] = ldg16(vp + voff + j * ld);
-        } else {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int row = min(kbase + 4 * vu + j, kend - 1) - kbase;
-                vreg[j] = ldg16(vp + row * ld + 8 * vv);
-            }
-        }
-    };
-    // K: rows of 256 bytes, 16-byte chunk c of key k at chunk c ^ (k mod 16).
-    // V^T: rows of 128 bytes (one per column d), 64 keys each in permuted
-    // order: key 32 s + kk sits at 32 s + 8 ((kk mod 16) / 4) + 4 (kk / 16) +
-    // kk mod 4; row d is stored at row vt_row(d), its 16-byte chunk c at chunk
-    // c ^ vt_swz(d).  With the lanes of a wave staging keys of both halves of
-    // a slice (vu = wave + 4 (lane / 16)), every 8-byte write instruction
-    // spreads evenly over the 64 banks and every fragment read is
-    // conflict-free (checked against the measured ds_read_b128 phases).
-    auto store_v = [&](int buf) {
-        uint8_t* Vl = lds + buf * 2 * kKvBytes + kKvBytes;
-        const int kp = 32 * (vu >> 3) + 8 * (vu & 3) + 4 * ((vu >> 2) & 1);  // permuted position of key 4u
-        const int cb = kp >> 3, ob = (kp & 7) * 2;
-#pragma unroll
-        for (int m = 0; m < 4; ++m) {
-            const uint32_t r0 = vreg[0][m], r1 = vreg[1][m], r2 = vreg[2][m], r3 = vreg[3][m];
-            const int d0 = 8 * vv + 2 * m, d1 = d0 + 1;
-            const uint2 e0 = make_uint2((r0 & 0xFFFFu) | (r1 << 16), (r2 & 0xFFFFu) | (r3 << 16));
-            const uint2 e1 = make_uint2((r0 >> 16) | (r1 & 0xFFFF0000u), (r2 >> 16) | (r3 & 0xFFFF0000u));
-            *(uint2*)(Vl + vt_row(d0) * 128 + ((cb ^ vt_swz(d0)) << 4) + ob) = e0;
-            *(uint2*)(Vl + vt_row(d1) * 128 + ((cb ^ vt_swz(d1)) << 4) + ob) = e1;
         }
     };
 
@@ -487,22 +466,21 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
     const float c2 = p.scale_log2;
     const float lazy = 8.0f / c2;  // 2^8 in probability, in units of raw scores
 
-    copy_k(0, 0);
-    load_v(0);
-    store_v(0);
-    // Every load of the prologue (the query fragments and the K copies
+    copy_kv(0, 0, false);
+    copy_kv(0, 0, true);
+    // Every load of the prologue (the query fragments and the K and V copies
     // included) has landed: the loop's waits then only cover the loads issued
     // inside the loop.
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     for (int kb = 0; kb < nkb; ++kb) {
         const int buf = kb & 1;
-        // The next block's loads, unconditionally (the last iteration reloads
-        // its own block into the other buffer, which nothing reads): a load
-        // that could reach the back-edge unconsumed would make the compiler
-        // wait for these loads in the middle of the matrix work.
-        copy_k(kb + 1 < nkb ? kb + 1 : kb, buf ^ 1);
-        load_v(kb + 1 < nkb ? kb + 1 : kb);
+        // The next block's copies into the other buffer, which every wave
+        // finished reading before the last barrier.
+        if (kb + 1 < nkb) {
+            copy_kv(kb + 1, buf ^ 1, false);
+            copy_kv(kb + 1, buf ^ 1, true);
+        }
         const int kbase = kb * kBk;
         // Every wave runs every block: one entirely above a wave's diagonal
         // (at most 2 of 4 waves, in the last block) is masked to zero weight,
@@ -584,16 +562,25 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs p) {
             for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
                 for (int dt = 0; dt < 8; ++dt) {
-                    const int d = dt * 16 + l16;
-                    const u32x4 vf = *(const u32x4*)(Vl + vt_row(d) * 128 + (((4 * ks + g) ^ vt_swz(d)) << 4));
+                    // lane (g, j) addresses key 32 ks + 16 t + 4 g + j/4,
+                    // columns 16 dt + 4 (j%4) .. + 3, and receives column
+                    // 16 dt + j of keys 32 ks + 16 t + 4 g + 0..3
+                    u32x4 vf;
+#pragma unroll
+                    for (int t = 0; t < 2; ++t) {
+                        const int key = 32 * ks + 16 * t + 4 * g + (l16 >> 2);
+                        const int c = 2 * dt + ((l16 & 3) >> 1);
+                        const uint2 u = lds_read_tr16(Vl + key * 256 + ((c ^ v_swz(key)) << 4) + 8 * (l16 & 1));
+                        vf[2 * t] = u.x;
+                        vf[2 * t + 1] = u.y;
+                    }
                     o[dt][0] = mfma_bf16(vf, pf[0][ks], o[dt][0]);
                     o[dt][1] = mfma_bf16(vf, pf[1][ks], o[dt][1]);
                 }
             }
         }
-        store_v(buf ^ 1);
-        // this wave's K copies into the other buffer (not tracked by the
-        // compiler) have landed before the barrier
+        // this wave's K and V copies into the other buffer (not tracked by
+        // the compiler) have landed before the barrier
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
     }
