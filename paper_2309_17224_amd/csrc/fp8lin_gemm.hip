@@ -594,11 +594,17 @@ __device__ __forceinline__ void gemm_tile(
             const uint32_t bc = canon_amax(b);  // the fold and the atomics take canonical NaNs
             if (AMAX && !bo.ws) atomicMax(amax_out, bc);
             if (AMAX && bo.ws) {
-                // The fold returns its old value, which is consumed before the
-                // count is issued, so the fold has been performed by then; the
-                // workgroup that counts last therefore sees every fold.
+                // The fold is a returning device-scope atomic whose result is
+                // consumed by an asm statement that also clobbers memory: the
+                // compiler cannot move the count above it, and the hardware
+                // has performed the fold (the wait for its return) before the
+                // count is issued.  The workgroup that counts last therefore
+                // finds every fold in ws[0].  A release/acquire count would
+                // say the same in the language's terms, but at agent scope
+                // its release writes back the XCD's L2 in every workgroup's
+                // epilogue (2-6 % slower on launches of several rounds).
                 const uint32_t prev = __hip_atomic_fetch_max(bo.ws, bc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                asm volatile("; fold returned %0" : : "v"(prev));
+                asm volatile("; fold returned %0" : : "v"(prev) : "memory");
                 const uint32_t done = __hip_atomic_fetch_add(bo.ws + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 if (done == gridDim.x - 1) {
                     const uint32_t a = __hip_atomic_exchange(bo.ws, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
