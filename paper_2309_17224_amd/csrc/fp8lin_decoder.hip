@@ -284,8 +284,8 @@ __global__ __launch_bounds__(kThreads) void swiglu_kernel(
 // Causal softmax attention for head dimension 128, one workgroup of 4 waves
 // per (query head, sequence, block of 128 queries); wave w owns queries
 // 32 w .. 32 w + 31 of the block as two tiles of 16.  Keys and values stream
-// through LDS in blocks of 64 (double buffered; the next block's global loads
-// are issued before the current block's matrix work).  Everything runs on
+// through LDS in blocks of 64 (double buffered; the next block's copies into
+// LDS are issued before the current block's matrix work).  Everything runs on
 // v_mfma_f32_16x16x32_bf16 in transposed form, so that no fragment needs a
 // shuffle between the two products:
 //   S^T = K . Q^T: A = key rows from LDS, B = query rows kept in registers;
